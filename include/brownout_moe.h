@@ -1,0 +1,216 @@
+/*
+ * brownout_moe.h -- C ABI of the grouped ("full-brownout") MoE layer forward
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The layer (paper: Sec. 2.1 for the top-K MoE layer, Eq. 1-2 in Sec. 4.2 for
+ * the expert-to-group map, the closing paragraphs of Sec. 4.3 and Sec. 4.4 for
+ * how the map is used while serving): a gate picks each token's top-k experts
+ * among E; a map g sends expert e to united expert g(e) of G; under full
+ * brownout every picked expert is served by its united expert. A token whose
+ * picks share a united expert calls it once with the sum of their gate
+ * weights. The output is
+ *
+ *     out_t = sum over distinct groups r of t's picks of gamma_{t,r} * FFN_r(x_t)
+ *             (+ shared-expert FFN(x_t) when the layer has shared experts)
+ *
+ * with FFN_r a SwiGLU expert, y = W_down (silu(W_gate a) * (W_up a)).
+ *
+ * Four calls make one forward, enqueued on one stream with no host sync:
+ *   brownout_moe_route     gate logits, softmax, top-k, map, per-group merge
+ *   brownout_moe_dispatch  per-group histogram, prefix, stable permutation, row gather
+ *   brownout_moe_ffn       grouped SwiGLU FFN over the united experts
+ *   brownout_moe_combine   gate-weighted sum back into token order
+ *
+ * Conventions for every call:
+ *   - Tensor pointers are DEVICE pointers, row-major, owned by the caller. The
+ *     library allocates nothing, frees nothing and keeps no state.
+ *   - Weights use the [out, in] layout: W_gate/W_up [n, d_ff, d], W_down [n, d, d_ff].
+ *   - Every call checks its arguments on the host before it enqueues anything;
+ *     on error it returns a BMOE_ERR_* code and writes nothing. Launch failures
+ *     return BMOE_ERR_HIP. Calls are asynchronous on `stream` (a hipStream_t;
+ *     NULL is the default stream); outputs are valid once the stream has
+ *     reached them.
+ *   - Pointers to float/bf16 tensors that kernels read or write 16 bytes at a
+ *     time (x, x_perm, w_*, h, y, out, y_shared) must be 16-byte aligned; d and
+ *     d_ff must be multiples of 8.
+ *   - T == 0 is a no-op that returns BMOE_OK.
+ *   - Inputs must be finite.
+ */
+#ifndef BROWNOUT_MOE_H
+#define BROWNOUT_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define BMOE_API __attribute__((visibility("default")))
+#else
+#define BMOE_API
+#endif
+
+#define BMOE_MAX_EXPERTS 256 /* E <= 256, hence G <= 256 */
+#define BMOE_MAX_TOPK 16     /* top_k <= 16 */
+
+/* Route decides every token whose fast fp32 logits leave any two of its top
+ * (k+1) values closer than this gap (2^-12) again from float64 logits; see
+ * brownout_moe_route. */
+#define BMOE_ROUTE_RECHECK_GAP (1.0f / 4096.0f)
+
+typedef enum bmoe_status {
+    BMOE_OK = 0,
+    BMOE_ERR_NULL = 1,        /* a required pointer is NULL                       */
+    BMOE_ERR_SHAPE = 2,       /* a size is out of range                            */
+    BMOE_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned                  */
+    BMOE_ERR_MAP = 4,         /* an expert-to-group map entry is outside [0, G)    */
+    BMOE_ERR_UNSUPPORTED = 5, /* unknown dtype, or a mode this build does not do  */
+    BMOE_ERR_WORKSPACE = 6,   /* workspace missing or too small                    */
+    BMOE_ERR_HIP = 7          /* the HIP runtime reported an error at launch       */
+} bmoe_status;
+
+typedef enum bmoe_dtype {
+    BMOE_F32 = 0,  /* float activations and weights                        */
+    BMOE_BF16 = 1  /* bf16 activations and weights, fp32 accumulation      */
+} bmoe_dtype;
+
+typedef enum bmoe_stage {
+    BMOE_STAGE_ROUTE = 0,
+    BMOE_STAGE_DISPATCH = 1,
+    BMOE_STAGE_FFN = 2,
+    BMOE_STAGE_COMBINE = 3
+} bmoe_stage;
+
+/* Shape of one layer. */
+typedef struct bmoe_desc {
+    int32_t T;           /* tokens, >= 0                                          */
+    int32_t d;           /* model width, multiple of 8                            */
+    int32_t E;           /* routed experts, 1..256                                */
+    int32_t top_k;       /* experts per token, 1..min(E, 16)                      */
+    int32_t G;           /* united experts (groups), 1..E                         */
+    int32_t d_ff;        /* SwiGLU width of a united expert, multiple of 8        */
+    int32_t d_ff_shared; /* width of the always-on shared FFN, 0 = none           */
+    int32_t norm_topk;   /* 1: the k gate weights are renormalised to sum to 1    */
+    int32_t dtype;       /* bmoe_dtype                                            */
+} bmoe_desc;
+
+/* Host-only checks (no HIP call). */
+BMOE_API bmoe_status bmoe_validate(const bmoe_desc* desc);
+/* e2g_host[E] (host memory): every entry in [0, G). The map is a static
+ * per-layer artifact (Sec. 4.3-4.4); kernels assume a validated map. */
+BMOE_API bmoe_status bmoe_validate_map(const int32_t* e2g_host, int32_t E, int32_t G);
+/* Workspace bytes a stage needs for `desc` (0: none). */
+BMOE_API size_t bmoe_workspace_bytes(const bmoe_desc* desc, int32_t stage);
+/* Static string for a status code. */
+BMOE_API const char* bmoe_status_str(bmoe_status status);
+/* Library version, e.g. 10000 for 1.0.0. */
+BMOE_API int32_t bmoe_version(void);
+
+/*
+ * brownout_moe_route -- the gate and the substitution by united experts.
+ * Paper: Sec. 2.1 (gating scores g_i of the top-K experts), Eq. 2 (the map),
+ * Sec. 4.3 last paragraph before Algorithm 1 (the gate still picks the
+ * experts; picked experts are replaced by their united expert).
+ *
+ *   z[t,e]   = x[t,:] . w_router[e,:] + bias[e]          (or logits_in[t,e])
+ *   p[t,:]   = softmax over all E of z[t,:]
+ *   slot i   = the i-th largest z[t,:] (ties: lower expert index first)
+ *   topk_idx[t,i] = that expert; topk_w[t,i] = its p (divided by the sum of
+ *                   the k values when desc->norm_topk)
+ *   slot_group[t,i] = e2g[topk_idx[t,i]] if no earlier slot of t has that
+ *                   group, else -1;
+ *   slot_gate[t,i]  = sum of topk_w[t,j] over j >= i with the same group when
+ *                   slot_group[t,i] >= 0, else 0.
+ *
+ * x [T,d] (dtype), w_router [E,d] (dtype), bias [E] float or NULL, e2g [E]
+ * int32 (validated map), logits_in [T,E] float or NULL. When logits_in is
+ * set, x, w_router and bias are not used (they may be NULL) and selection
+ * runs on those exact values.
+ * Otherwise the logits are computed in fp32 (bf16: MFMA); a token whose fp32
+ * top-(k+1) values have an adjacent gap below BMOE_ROUTE_RECHECK_GAP has its
+ * candidate experts re-evaluated in float64 and is selected on those.
+ * Outputs: topk_idx, slot_group [T,k] int32; topk_w, slot_gate [T,k] float;
+ * logits_out [T,E] float or NULL (the fp32 logits, bias included).
+ * No workspace.
+ */
+BMOE_API bmoe_status brownout_moe_route(const bmoe_desc* desc, const void* x, const void* w_router,
+                               const float* bias, const float* logits_in, const int32_t* e2g,
+                               int32_t* topk_idx, float* topk_w, int32_t* slot_group,
+                               float* slot_gate, float* logits_out, void* stream);
+
+/*
+ * brownout_moe_dispatch -- group rows for the united experts (Eq. 2: the sets
+ * G_r of the map, here filled with (token, group) pairs).
+ *
+ *   counts[r]   = number of tokens with a valid slot of group r
+ *   offsets     = exclusive prefix of counts, offsets[G] = N (total rows)
+ *   rows of group r are offsets[r] .. offsets[r+1]-1, in ascending token order
+ *   perm_token[row] = token of that row; slot_row[t,i] = row of slot (t,i), or -1
+ *   x_perm[row,:]   = x[perm_token[row],:]  (bit copy)
+ *
+ * slot_group [T,k] int32 as written by brownout_moe_route (entries outside
+ * [-1, G) count as -1). x [T,d] (dtype). counts [G], offsets [G+1],
+ * perm_token [T*k], slot_row [T,k] int32; x_perm [T*k, d] (dtype). Rows at
+ * and beyond N are left unspecified.
+ * workspace: bmoe_workspace_bytes(desc, BMOE_STAGE_DISPATCH) bytes, 256-byte
+ * aligned, ALL ZERO before the first call that uses it; every call leaves it
+ * all zero again when it completes on the stream. Two calls that share a
+ * workspace must not overlap in time.
+ * Implementation: a histogram with LDS atomics and a single-pass decoupled
+ * look-back scan across token tiles, then a 128-bit row gather.
+ */
+BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t* slot_group,
+                                  const void* x, int32_t* counts, int32_t* offsets,
+                                  int32_t* perm_token, int32_t* slot_row, void* x_perm,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * brownout_moe_ffn -- grouped SwiGLU FFN (Sec. 2.1 "small FFNs"; SwiGLU form).
+ * Segment s covers rows offsets[s] .. offsets[s+1]-1 of a and uses united
+ * expert s:
+ *   h[row,:] = silu(a[row,:] W_gate[s]^T) * (a[row,:] W_up[s]^T)   (stored in dtype)
+ *   y[row,:] = h[row,:] W_down[s]^T                                  (stored in dtype)
+ * dtype: bmoe_dtype. offsets [n_seg+1] int32 in DEVICE memory (as written by
+ * dispatch; non-decreasing, offsets[n_seg] <= rows_cap; rows beyond rows_cap
+ * are never touched). a [rows_cap, d]; w_gate, w_up [n_seg, d_ff, d];
+ * w_down [n_seg, d, d_ff]; h [rows_cap, d_ff] (scratch the caller owns);
+ * y [rows_cap, d]. n_seg in 1..256. bf16: MFMA, fp32 accumulation.
+ * The shared experts of a layer run through this call too, with n_seg = 1,
+ * offsets = {0, T}, a = x.
+ */
+BMOE_API bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                             int32_t d_ff, const int32_t* offsets, const void* a,
+                             const void* w_gate, const void* w_up, const void* w_down, void* h,
+                             void* y, void* stream);
+
+/* The two grouped GEMMs of brownout_moe_ffn, callable on their own (same
+ * arguments and rules as brownout_moe_ffn):
+ *   brownout_moe_ffn_gate_up: h = silu(a W_gate[s]^T) * (a W_up[s]^T)
+ *   brownout_moe_ffn_down:    y = h W_down[s]^T                                   */
+BMOE_API bmoe_status brownout_moe_ffn_gate_up(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                     int32_t d_ff, const int32_t* offsets, const void* a,
+                                     const void* w_gate, const void* w_up, void* h, void* stream);
+BMOE_API bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                  int32_t d_ff, const int32_t* offsets, const void* h,
+                                  const void* w_down, void* y, void* stream);
+
+/*
+ * brownout_moe_combine -- weighted sum back into token order (Sec. 2.1: the
+ * layer output is the gate-weighted sum of the expert outputs).
+ *   out[t,:] = sum over i ascending with slot_row[t,i] >= 0 of
+ *              slot_gate[t,i] * y_perm[slot_row[t,i],:]  (+ y_shared[t,:])
+ * fp32 accumulation, stored in dtype. slot_row [T,k] int32, slot_gate [T,k]
+ * float, y_perm [T*k, d], y_shared [T,d] or NULL, out [T,d]. Rows of y_perm
+ * named by slot_row must be < T*k.
+ */
+BMOE_API bmoe_status brownout_moe_combine(const bmoe_desc* desc, const int32_t* slot_row,
+                                 const float* slot_gate, const void* y_perm,
+                                 const void* y_shared, void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BROWNOUT_MOE_H */

@@ -1,0 +1,352 @@
+"""Python binding of libbrownout_moe (argument marshalling only).
+
+Every function here checks tensor placement/dtype/shape, passes raw device
+pointers and the current HIP stream to the C ABI declared in
+``include/brownout_moe.h``, and raises ``BmoeError`` on a non-OK status. All
+arithmetic runs in the library's HIP kernels; torch provides device memory and
+streams. There is no fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbrownout_moe.so")
+
+BMOE_F32, BMOE_BF16 = 0, 1
+STAGE_ROUTE, STAGE_DISPATCH, STAGE_FFN, STAGE_COMBINE = 0, 1, 2, 3
+ROUTE_RECHECK_GAP = 1.0 / 4096.0
+MAX_EXPERTS, MAX_TOPK = 256, 16
+
+STATUS = {0: "BMOE_OK", 1: "BMOE_ERR_NULL", 2: "BMOE_ERR_SHAPE", 3: "BMOE_ERR_ALIGN",
+          4: "BMOE_ERR_MAP", 5: "BMOE_ERR_UNSUPPORTED", 6: "BMOE_ERR_WORKSPACE", 7: "BMOE_ERR_HIP"}
+
+EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_status_str",
+            "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
+            "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine")
+
+
+class BmoeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({status_str(status)})")
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("G", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+                ("d_ff_shared", ctypes.c_int32), ("norm_topk", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == BMOE_BF16 else torch.float32
+
+    def replace(self, **kw) -> "Desc":
+        vals = {f: getattr(self, f) for f, _ in self._fields_}
+        vals.update(kw)
+        return Desc(**vals)
+
+
+def make_desc(T, d, E, top_k, G, d_ff, d_ff_shared=0, norm_topk=0, dtype="bf16") -> Desc:
+    dt = {"bf16": BMOE_BF16, "f32": BMOE_F32, BMOE_BF16: BMOE_BF16, BMOE_F32: BMOE_F32}[dtype]
+    return Desc(int(T), int(d), int(E), int(top_k), int(G), int(d_ff), int(d_ff_shared),
+                int(norm_topk), dt)
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it first (python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    DP = ctypes.POINTER(Desc)
+    lib.bmoe_validate.argtypes = [DP]
+    lib.bmoe_validate.restype = I32
+    lib.bmoe_validate_map.argtypes = [P, I32, I32]
+    lib.bmoe_validate_map.restype = I32
+    lib.bmoe_workspace_bytes.argtypes = [DP, I32]
+    lib.bmoe_workspace_bytes.restype = SZ
+    lib.bmoe_status_str.argtypes = [I32]
+    lib.bmoe_status_str.restype = ctypes.c_char_p
+    lib.bmoe_version.restype = I32
+    lib.brownout_moe_route.argtypes = [DP] + [P] * 11
+    lib.brownout_moe_route.restype = I32
+    lib.brownout_moe_dispatch.argtypes = [DP] + [P] * 8 + [SZ, P]
+    lib.brownout_moe_dispatch.restype = I32
+    lib.brownout_moe_ffn.argtypes = [I32] * 5 + [P] * 8
+    lib.brownout_moe_ffn.restype = I32
+    lib.brownout_moe_ffn_gate_up.argtypes = [I32] * 5 + [P] * 6
+    lib.brownout_moe_ffn_gate_up.restype = I32
+    lib.brownout_moe_ffn_down.argtypes = [I32] * 5 + [P] * 5
+    lib.brownout_moe_ffn_down.restype = I32
+    lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
+    lib.brownout_moe_combine.restype = I32
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load_library().bmoe_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise BmoeError(status, where)
+
+
+def validate(desc: Desc) -> int:
+    return int(load_library().bmoe_validate(ctypes.byref(desc)))
+
+
+def validate_map(e2g_host, E: int, G: int) -> int:
+    import numpy as np
+    a = np.ascontiguousarray(e2g_host, dtype=np.int32)
+    return int(load_library().bmoe_validate_map(a.ctypes.data_as(ctypes.c_void_p), int(E), int(G)))
+
+
+def workspace_bytes(desc: Desc, stage: int) -> int:
+    return int(load_library().bmoe_workspace_bytes(ctypes.byref(desc), int(stage)))
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+# ---------------------------------------------------------------------------
+# the four calls
+
+def route(desc: Desc, x: Optional[torch.Tensor], w_router: Optional[torch.Tensor],
+          bias: Optional[torch.Tensor], e2g: torch.Tensor, *, logits_in: Optional[torch.Tensor] = None,
+          want_logits: bool = False, out: Optional[Dict[str, torch.Tensor]] = None,
+          stream=None) -> Dict[str, torch.Tensor]:
+    T, E, k = desc.T, desc.E, desc.top_k
+    dev = e2g.device
+    _dev(e2g, "e2g", torch.int32, (E,))
+    if logits_in is None:
+        _dev(x, "x", desc.torch_dtype, (T, desc.d))
+        _dev(w_router, "w_router", desc.torch_dtype, (E, desc.d))
+        if bias is not None:
+            _dev(bias, "bias", torch.float32, (E,))
+    else:
+        _dev(logits_in, "logits_in", torch.float32, (T, E))
+    o = dict(out) if out else {}
+    o.setdefault("topk_idx", _empty((T, k), torch.int32, dev))
+    o.setdefault("topk_w", _empty((T, k), torch.float32, dev))
+    o.setdefault("slot_group", _empty((T, k), torch.int32, dev))
+    o.setdefault("slot_gate", _empty((T, k), torch.float32, dev))
+    if want_logits:
+        o.setdefault("logits", _empty((T, E), torch.float32, dev))
+    st = load_library().brownout_moe_route(
+        ctypes.byref(desc), _p(x), _p(w_router), _p(bias), _p(logits_in), _p(e2g), _p(o["topk_idx"]),
+        _p(o["topk_w"]), _p(o["slot_group"]), _p(o["slot_gate"]), _p(o.get("logits")), _stream(stream))
+    _check(st, "brownout_moe_route")
+    return o
+
+
+def dispatch(desc: Desc, slot_group: torch.Tensor, x: torch.Tensor, workspace: torch.Tensor, *,
+             out: Optional[Dict[str, torch.Tensor]] = None, stream=None) -> Dict[str, torch.Tensor]:
+    T, k, G, d = desc.T, desc.top_k, desc.G, desc.d
+    dev = x.device
+    _dev(slot_group, "slot_group", torch.int32, (T, k))
+    _dev(x, "x", desc.torch_dtype, (T, d))
+    _dev(workspace, "workspace")
+    o = dict(out) if out else {}
+    o.setdefault("counts", _empty((G,), torch.int32, dev))
+    o.setdefault("offsets", _empty((G + 1,), torch.int32, dev))
+    o.setdefault("perm_token", _empty((max(T * k, 1),), torch.int32, dev))
+    o.setdefault("slot_row", _empty((T, k), torch.int32, dev))
+    o.setdefault("x_perm", _empty((max(T * k, 1), d), desc.torch_dtype, dev))
+    st = load_library().brownout_moe_dispatch(
+        ctypes.byref(desc), _p(slot_group), _p(x), _p(o["counts"]), _p(o["offsets"]),
+        _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]), _p(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "brownout_moe_dispatch")
+    return o
+
+
+def new_dispatch_workspace(desc: Desc, device) -> torch.Tensor:
+    """An all-zero workspace of the size dispatch needs (kept zero by every call)."""
+    n = workspace_bytes(desc, STAGE_DISPATCH)
+    return torch.zeros((n + 255) // 256 * 256, dtype=torch.uint8, device=device)
+
+
+def _ffn_checks(offsets, a_rows, dt, n_seg, d, d_ff):
+    dtype = {torch.bfloat16: BMOE_BF16, torch.float32: BMOE_F32}.get(dt)
+    if dtype is None:
+        raise ValueError(f"unsupported dtype {dt}")
+    _dev(offsets, "offsets", torch.int32, (n_seg + 1,))
+    return dtype
+
+
+def ffn(offsets: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
+        w_down: torch.Tensor, *, h: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
+        stream=None):
+    """Both grouped GEMMs: returns (y, h)."""
+    n_seg, d_ff, d = w_gate.shape
+    rows_cap, dt = a.shape[0], a.dtype
+    dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
+    _dev(a, "a", dt, (rows_cap, d))
+    _dev(w_gate, "w_gate", dt, (n_seg, d_ff, d))
+    _dev(w_up, "w_up", dt, (n_seg, d_ff, d))
+    _dev(w_down, "w_down", dt, (n_seg, d, d_ff))
+    h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
+    y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, a.device)
+    st = load_library().brownout_moe_ffn(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a), _p(w_gate),
+                                         _p(w_up), _p(w_down), _p(h), _p(y), _stream(stream))
+    _check(st, "brownout_moe_ffn")
+    return y, h
+
+
+def ffn_gate_up(offsets, a, w_gate, w_up, *, h=None, stream=None):
+    n_seg, d_ff, d = w_gate.shape
+    rows_cap, dt = a.shape[0], a.dtype
+    dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
+    _dev(a, "a", dt, (rows_cap, d))
+    _dev(w_gate, "w_gate", dt, (n_seg, d_ff, d))
+    _dev(w_up, "w_up", dt, (n_seg, d_ff, d))
+    h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
+    st = load_library().brownout_moe_ffn_gate_up(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a),
+                                                 _p(w_gate), _p(w_up), _p(h), _stream(stream))
+    _check(st, "brownout_moe_ffn_gate_up")
+    return h
+
+
+def ffn_down(offsets, h, w_down, *, y=None, stream=None):
+    n_seg, d, d_ff = w_down.shape
+    rows_cap, dt = h.shape[0], h.dtype
+    dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
+    _dev(h, "h", dt, (rows_cap, d_ff))
+    _dev(w_down, "w_down", dt, (n_seg, d, d_ff))
+    y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, h.device)
+    st = load_library().brownout_moe_ffn_down(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(h),
+                                              _p(w_down), _p(y), _stream(stream))
+    _check(st, "brownout_moe_ffn_down")
+    return y
+
+
+def combine(desc: Desc, slot_row: torch.Tensor, slot_gate: torch.Tensor, y_perm: torch.Tensor,
+            y_shared: Optional[torch.Tensor] = None, *, out: Optional[torch.Tensor] = None, stream=None):
+    T, k, d = desc.T, desc.top_k, desc.d
+    _dev(slot_row, "slot_row", torch.int32, (T, k))
+    _dev(slot_gate, "slot_gate", torch.float32, (T, k))
+    _dev(y_perm, "y_perm", desc.torch_dtype)
+    if y_perm.shape[0] < T * k or y_perm.shape[1] != d:
+        raise ValueError("y_perm must be [>= T*k, d]")
+    if y_shared is not None:
+        _dev(y_shared, "y_shared", desc.torch_dtype, (T, d))
+    out = _dev(out, "out", desc.torch_dtype, (T, d)) if out is not None else _empty((T, d), desc.torch_dtype, slot_row.device)
+    st = load_library().brownout_moe_combine(ctypes.byref(desc), _p(slot_row), _p(slot_gate), _p(y_perm),
+                                             _p(y_shared), _p(out), _stream(stream))
+    _check(st, "brownout_moe_combine")
+    return out
+
+
+# ---------------------------------------------------------------------------
+
+class LayerForward:
+    """One grouped MoE layer with its weights and every intermediate buffer
+    allocated once, so a forward enqueues only the library's kernels.
+
+    weights: dict with w_router [E,d], bias [E] (float or None), e2g [E] int32,
+    w_gate/w_up [G,d_ff,d], w_down [G,d,d_ff], and optionally w_gate_sh/w_up_sh
+    [1,d_ff_shared,d], w_down_sh [1,d,d_ff_shared] (all device tensors).
+    """
+
+    def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda"):
+        self.desc = desc
+        self.w = weights
+        _check(validate(desc), "bmoe_validate")
+        T, k, d, G, E = desc.T, desc.top_k, desc.d, desc.G, desc.E
+        dt = desc.torch_dtype
+        rows = max(T * k, 1)
+        self.bufs = {
+            "route": {n: _empty((T, k), t, device) for n, t in
+                      (("topk_idx", torch.int32), ("topk_w", torch.float32),
+                       ("slot_group", torch.int32), ("slot_gate", torch.float32))},
+            "dispatch": {"counts": _empty((G,), torch.int32, device),
+                         "offsets": _empty((G + 1,), torch.int32, device),
+                         "perm_token": _empty((rows,), torch.int32, device),
+                         "slot_row": _empty((T, k), torch.int32, device),
+                         "x_perm": _empty((rows, d), dt, device)},
+            "h": _empty((rows, desc.d_ff), dt, device),
+            "y": _empty((rows, d), dt, device),
+            "out": _empty((T, d), dt, device),
+        }
+        self.ws = new_dispatch_workspace(desc, device)
+        if desc.d_ff_shared:
+            self.bufs["h_sh"] = _empty((max(T, 1), desc.d_ff_shared), dt, device)
+            self.bufs["y_sh"] = _empty((max(T, 1), d), dt, device)
+            self.sh_offsets = torch.tensor([0, T], dtype=torch.int32, device=device)
+
+    def route(self, x, stream=None):
+        w = self.w
+        return route(self.desc, x, w["w_router"], w.get("bias"), w["e2g"], out=self.bufs["route"],
+                     stream=stream)
+
+    def dispatch(self, x, stream=None):
+        return dispatch(self.desc, self.bufs["route"]["slot_group"], x, self.ws,
+                        out=self.bufs["dispatch"], stream=stream)
+
+    def ffn(self, stream=None):
+        w = self.w
+        return ffn(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
+                   w["w_up"], w["w_down"], h=self.bufs["h"], y=self.bufs["y"], stream=stream)
+
+    def ffn_gate_up(self, stream=None):
+        w = self.w
+        return ffn_gate_up(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
+                           w["w_up"], h=self.bufs["h"], stream=stream)
+
+    def ffn_down(self, stream=None):
+        return ffn_down(self.bufs["dispatch"]["offsets"], self.bufs["h"], self.w["w_down"],
+                        y=self.bufs["y"], stream=stream)
+
+    def shared(self, x, stream=None):
+        w = self.w
+        return ffn(self.sh_offsets, x, w["w_gate_sh"], w["w_up_sh"], w["w_down_sh"],
+                   h=self.bufs["h_sh"], y=self.bufs["y_sh"], stream=stream)
+
+    def combine(self, stream=None):
+        y_sh = self.bufs["y_sh"] if self.desc.d_ff_shared else None
+        return combine(self.desc, self.bufs["dispatch"]["slot_row"], self.bufs["route"]["slot_gate"],
+                       self.bufs["y"], y_sh, out=self.bufs["out"], stream=stream)
+
+    def __call__(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        self.route(x, stream)
+        self.dispatch(x, stream)
+        self.ffn(stream)
+        if self.desc.d_ff_shared:
+            self.shared(x, stream)
+        return self.combine(stream)

@@ -1,0 +1,128 @@
+// Internal helpers shared by the HIP kernels of libbrownout_moe (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "brownout_moe.h"
+
+namespace bmoe {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// float -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// 16x16x32 bf16 MFMA: lane l holds A[l%16][8*(l/16)+j], B[8*(l/16)+j][l%16];
+// result D[4*(l/16)+i][l%16] in element i.
+__device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+// 32x32x16 bf16 MFMA: lane l holds A[l%32][8*(l/32)+j], B[8*(l/32)+j][l%32];
+// result D[8*(i/4)+4*(l/32)+i%4][l%32] in element i.
+__device__ __forceinline__ f32x16 mfma32(const uint4& a, const uint4& b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+__host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ constexpr int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Block-wide exclusive scan of up to 256 ints held one per thread (blockDim = 256).
+// `buf` is 256 ints of LDS. Returns the exclusive prefix; *total gets the sum.
+__device__ __forceinline__ int block_exclusive_scan_256(int v, int* buf, int* total) {
+    const int tid = threadIdx.x;
+    buf[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        int add = tid >= off ? buf[tid - off] : 0;
+        __syncthreads();
+        buf[tid] += add;
+        __syncthreads();
+    }
+    int incl = buf[tid];
+    *total = buf[255];
+    __syncthreads();
+    return incl - v;
+}
+
+}  // namespace bmoe
+
+// Launchers implemented by the kernel files; arguments already validated.
+namespace bmoe {
+
+struct RouteArgs {
+    const void* x;
+    const void* w;
+    const float* bias;
+    const float* logits_in;
+    const int32_t* e2g;
+    int32_t* topk_idx;
+    float* topk_w;
+    int32_t* slot_group;
+    float* slot_gate;
+    float* logits_out;
+    int T, d, E, k, G, norm, dtype;
+};
+hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+
+struct DispatchArgs {
+    const int32_t* slot_group;
+    const void* x;
+    int32_t* counts;
+    int32_t* offsets;
+    int32_t* perm_token;
+    int32_t* slot_row;
+    void* x_perm;
+    void* ws;
+    int T, d, k, G, elem_bytes;
+};
+size_t dispatch_ws_bytes(int T, int G);
+hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);
+
+struct FfnArgs {
+    const int32_t* offsets;
+    const void* a;
+    const void* w_gate;
+    const void* w_up;
+    const void* w_down;
+    void* h;
+    void* y;
+    int n_seg, rows_cap, d, d_ff, dtype;
+};
+// part: 0 = both GEMMs, 1 = gate/up only, 2 = down only
+hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part = 0);
+
+struct CombineArgs {
+    const int32_t* slot_row;
+    const float* slot_gate;
+    const void* y;
+    const void* y_shared;
+    void* out;
+    int T, k, d, elem_bytes;
+    int64_t rows_cap;
+};
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+
+}  // namespace bmoe

@@ -1,0 +1,223 @@
+// Group rows for the united experts: the sets G_r of the map (Eq. 2) filled
+// with (token, group) pairs, in ascending token order within a group.
+//
+// Kernel 1 (hist_scan), one workgroup per tile of 256 tokens, tiles numbered
+// by an atomic ticket in start order:
+//   - each valid slot sets its token's bit in a per-group 256-bit LDS mask
+//     (LDS atomic OR); popcounts give the tile's group counts and every
+//     slot's stable rank inside the tile;
+//   - single-pass decoupled look-back: the tile publishes its counts, walks
+//     back over earlier tiles' published counts / inclusive prefixes until it
+//     meets a prefix, then publishes its own inclusive prefix;
+//   - slot_row receives the row relative to the group start; the last tile
+//     writes the group counts and their exclusive prefix (offsets).
+// Kernel 2 (permute), one wave per token: adds offsets[group] to the relative
+// row, writes perm_token, and copies x[t] into each of its rows with 128-bit
+// loads and stores. Workgroup 0 clears the look-back state for the next call.
+#include "bmoe_common.h"
+
+namespace bmoe {
+namespace {
+
+constexpr int kTile = 256;
+constexpr uint32_t kFlagAgg = 1u, kFlagPrefix = 2u;
+// Upper bound on polls of one predecessor's status word. Predecessors publish
+// without waiting, so the bound is only reached if the workspace was not
+// zeroed before the first call; the walk then gives up instead of hanging.
+constexpr int kMaxPolls = 1 << 22;
+
+struct DispatchWs {
+    int32_t ticket;
+    int32_t pad[63];
+    // followed by uint64_t status[ntiles * G]
+};
+
+__device__ __forceinline__ uint64_t pack_status(uint32_t flag, uint32_t value) {
+    return ((uint64_t)flag << 32) | value;
+}
+
+__global__ __launch_bounds__(kTile) void hist_scan_kernel(const int32_t* __restrict__ slot_group,
+                                                          int32_t* __restrict__ slot_row,
+                                                          int32_t* __restrict__ counts,
+                                                          int32_t* __restrict__ offsets, void* ws,
+                                                          int T, int k, int G, int ntiles) {
+    __shared__ unsigned long long masks[BMOE_MAX_EXPERTS][kTile / 64];
+    __shared__ int s_tile;
+    __shared__ int s_excl[BMOE_MAX_EXPERTS];
+    __shared__ int s_cnt[BMOE_MAX_EXPERTS];
+    __shared__ int s_scan[256];
+    DispatchWs* hdr = (DispatchWs*)ws;
+    uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
+    const int tid = threadIdx.x;
+
+    if (tid == 0) s_tile = atomicAdd(&hdr->ticket, 1);
+    for (int g = tid; g < G; g += kTile) {
+#pragma unroll
+        for (int w = 0; w < kTile / 64; ++w) masks[g][w] = 0ull;
+    }
+    __syncthreads();
+    const int tile = s_tile;
+    if (tile >= ntiles) return;  // workspace not zeroed: no out-of-range writes
+    const int t = tile * kTile + tid;
+    const bool tok = t < T;
+
+    int grp[BMOE_MAX_TOPK];
+#pragma unroll
+    for (int i = 0; i < BMOE_MAX_TOPK; ++i) {
+        grp[i] = -1;
+        if (i < k && tok) {
+            int g = slot_group[(size_t)t * k + i];
+            if (g >= 0 && g < G) {
+                grp[i] = g;
+                atomicOr(&masks[g][tid >> 6], 1ull << (tid & 63));
+            }
+        }
+    }
+    __syncthreads();
+
+    if (tid < G) {
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < kTile / 64; ++w) c += __popcll(masks[tid][w]);
+        s_cnt[tid] = c;
+        uint64_t* my = status + (size_t)tile * G + tid;
+        int excl = 0;
+        if (tile == 0) {
+            __hip_atomic_store(my, pack_status(kFlagPrefix, (uint32_t)c), __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            __hip_atomic_store(my, pack_status(kFlagAgg, (uint32_t)c), __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            // look back; every earlier tile took its ticket before this one and
+            // publishes without waiting on anything, so the walk terminates
+            int j = tile - 1;
+            int polls = 0;
+            while (true) {
+                uint64_t sv = __hip_atomic_load(status + (size_t)j * G + tid, __ATOMIC_ACQUIRE,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+                uint32_t flag = (uint32_t)(sv >> 32);
+                if (flag == 0u) {
+                    if (++polls > kMaxPolls) break;
+                    __builtin_amdgcn_s_sleep(1);
+                    continue;
+                }
+                polls = 0;
+                excl += (int)(uint32_t)sv;
+                if (flag == kFlagPrefix) break;
+                --j;
+            }
+            __hip_atomic_store(my, pack_status(kFlagPrefix, (uint32_t)(excl + c)), __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        s_excl[tid] = excl;
+    }
+    __syncthreads();
+
+    if (tok) {
+        const int w = tid >> 6;
+        const unsigned long long lt = (1ull << (tid & 63)) - 1ull;
+#pragma unroll
+        for (int i = 0; i < BMOE_MAX_TOPK; ++i) {
+            if (i < k) {
+                int rel = -1;
+                const int g = grp[i];
+                if (g >= 0) {
+                    int rank = __popcll(masks[g][w] & lt);
+                    for (int ww = 0; ww < w; ++ww) rank += __popcll(masks[g][ww]);
+                    rel = s_excl[g] + rank;
+                }
+                slot_row[(size_t)t * k + i] = rel;
+            }
+        }
+    }
+
+    if (tile == ntiles - 1) {
+        const int total = tid < G ? s_excl[tid] + s_cnt[tid] : 0;
+        int sum;
+        const int ex = block_exclusive_scan_256(total, s_scan, &sum);
+        if (tid < G) {
+            counts[tid] = total;
+            offsets[tid] = ex;
+        }
+        if (tid == 0) offsets[G] = sum;
+    }
+}
+
+// One wave per token. VEC: 16-byte chunks each lane moves per batch.
+template <int VEC>
+__global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict__ slot_group,
+                                                      int32_t* __restrict__ slot_row,
+                                                      const int32_t* __restrict__ offsets,
+                                                      int32_t* __restrict__ perm_token,
+                                                      const uint4* __restrict__ x,
+                                                      uint4* __restrict__ x_perm, void* ws, int T,
+                                                      int k, int G, int nch, int ntiles, int rows_cap) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    if (blockIdx.x == 0) {
+        // leave the look-back state all zero for the next call
+        DispatchWs* hdr = (DispatchWs*)ws;
+        uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
+        const int n = ntiles * G;
+        for (int i = tid; i < n; i += 256) status[i] = 0ull;
+        if (tid == 0) hdr->ticket = 0;
+    }
+    const int t = blockIdx.x * 4 + (tid >> 6);
+    if (t >= T) return;
+    int row = -1;
+    if (lane < k) {
+        const size_t o = (size_t)t * k + lane;
+        const int g = slot_group[o];
+        if (g >= 0 && g < G) {
+            row = offsets[g] + slot_row[o];
+            if (row < 0 || row >= rows_cap) row = -1;
+            else perm_token[row] = t;
+        }
+        slot_row[o] = row;
+    }
+    const uint4* src = x + (size_t)t * nch;
+    int rows[BMOE_MAX_TOPK];
+#pragma unroll
+    for (int i = 0; i < BMOE_MAX_TOPK; ++i) rows[i] = i < k ? __shfl(row, i) : -1;
+    for (int c0 = lane; c0 < nch; c0 += 64 * VEC) {
+        uint4 v[VEC];
+#pragma unroll
+        for (int u = 0; u < VEC; ++u) {
+            const int c = c0 + 64 * u;
+            v[u] = src[c < nch ? c : 0];
+        }
+#pragma unroll
+        for (int i = 0; i < BMOE_MAX_TOPK; ++i) {
+            if (rows[i] >= 0) {
+                uint4* dst = x_perm + (size_t)rows[i] * nch;
+#pragma unroll
+                for (int u = 0; u < VEC; ++u) {
+                    const int c = c0 + 64 * u;
+                    if (c < nch) dst[c] = v[u];
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+size_t dispatch_ws_bytes(int T, int G) {
+    const size_t ntiles = (size_t)ceil_div(T > 0 ? T : 1, kTile);
+    return sizeof(DispatchWs) + ntiles * (size_t)G * sizeof(uint64_t);
+}
+
+hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
+    if (a.T == 0) return hipSuccess;
+    const int ntiles = ceil_div(a.T, kTile);
+    hipLaunchKernelGGL(hist_scan_kernel, dim3(ntiles), dim3(kTile), 0, s, a.slot_group, a.slot_row,
+                       a.counts, a.offsets, a.ws, a.T, a.k, a.G, ntiles);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int nch = a.d * a.elem_bytes / 16;
+    hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                       a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
+                       a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
+    return hipGetLastError();
+}
+
+}  // namespace bmoe

@@ -36,6 +36,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Dict, Optional
 
 import numpy as np
@@ -101,22 +102,34 @@ def scaled(cfg: LayerConfig, **kw) -> LayerConfig:
 # ---------------------------------------------------------------------------
 # bf16 helpers (storage format only)
 
+def _bf16_chunk(c: np.ndarray) -> np.ndarray:
+    lsb = (c >> 16) & 1
+    r = (c + np.uint32(0x7FFF) + lsb) >> 16
+    nan = (c & 0x7FFFFFFF) > 0x7F800000
+    if nan.any():
+        r = np.where(nan, (c >> 16) | 0x40, r)
+    return r.astype(np.uint16)
+
+
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round float32 to bf16 with round-to-nearest-even; returns uint16 bit patterns."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32)
+    flat_u = a.view(np.uint32).reshape(-1)
     out = np.empty(a.shape, dtype=np.uint16)
-    # process in chunks to bound temporaries on multi-GB tensors
-    flat_u, flat_o = u.reshape(-1), out.reshape(-1)
-    step = 1 << 24
-    for s in range(0, flat_u.size, step):
-        c = flat_u[s:s + step]
-        lsb = (c >> 16) & 1
-        r = (c + np.uint32(0x7FFF) + lsb) >> 16
-        nan = (c & 0x7FFFFFFF) > 0x7F800000
-        if nan.any():
-            r = np.where(nan, (c >> 16) | 0x40, r)
-        flat_o[s:s + step] = r.astype(np.uint16)
+    flat_o = out.reshape(-1)
+    step = 1 << 22
+    starts = range(0, flat_u.size, step)
+
+    def work(s):
+        flat_o[s:s + step] = _bf16_chunk(flat_u[s:s + step])
+
+    if flat_u.size <= step:
+        for s in starts:
+            work(s)
+    else:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(work, starts))
     return out
 
 

@@ -1,0 +1,138 @@
+"""The C ABI on the host (no GPU): the library loads, exports every function
+the public header declares, and rejects bad arguments before any HIP call.
+Every call here fails host validation (or is the T == 0 no-op), so nothing is
+ever enqueued."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_04164_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "brownout_moe.h")
+
+OK, NULL, SHAPE, ALIGN, MAP, UNSUP, WS = 0, 1, 2, 3, 4, 5, 6
+FAKE = ctypes.c_void_p(0x10000)      # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p(0x10008)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"BMOE_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)))
+
+
+def good_desc(**kw):
+    d = B.make_desc(T=64, d=256, E=8, top_k=2, G=4, d_ff=512, dtype="bf16")
+    return d.replace(**kw) if kw else d
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 11, names
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in the header but not exported"
+    assert set(names) == set(B.EXPORTED)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.bmoe_version() == 10000
+    for s in range(8):
+        assert len(B.status_str(s)) >= 2
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("T", -1, SHAPE), ("E", 0, SHAPE), ("E", 257, SHAPE), ("top_k", 0, SHAPE), ("top_k", 9, SHAPE),
+    ("G", 0, SHAPE), ("G", 9, SHAPE), ("d", 12, SHAPE), ("d", 0, SHAPE), ("d_ff", 20, SHAPE),
+    ("d_ff_shared", 4, SHAPE), ("d_ff_shared", -8, SHAPE), ("norm_topk", 2, SHAPE), ("dtype", 3, UNSUP),
+])
+def test_validate_rejects(field, value, code):
+    assert B.validate(good_desc(**{field: value})) == code
+
+
+def test_validate_accepts_configs():
+    from paper_2607_04164_amd import workload as W
+    for cfg in W.CONFIGS.values():
+        d = B.make_desc(cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.G, cfg.d_ff, cfg.d_ff_shared,
+                        cfg.norm_topk, cfg.dtype)
+        assert B.validate(d) == OK, cfg.name
+    assert B.validate(good_desc(E=256, top_k=16, G=256)) == OK
+    assert B.validate(good_desc(top_k=17, E=64)) == SHAPE
+
+
+def test_validate_map():
+    assert B.validate_map([0, 1, 2, 3, 0, 1, 2, 3], 8, 4) == OK
+    assert B.validate_map([0, 1, 2, 4, 0, 1, 2, 3], 8, 4) == MAP
+    assert B.validate_map([0, -1, 2, 3, 0, 1, 2, 3], 8, 4) == MAP
+    assert B.validate_map([0, 0], 2, 3) == SHAPE
+
+
+def test_workspace_bytes():
+    d = good_desc(T=1000, E=16, G=16)
+    n = B.workspace_bytes(d, B.STAGE_DISPATCH)
+    assert n == 256 + 4 * 16 * 8  # header + ceil(1000/256) tiles x G status words
+    for st in (B.STAGE_ROUTE, B.STAGE_FFN, B.STAGE_COMBINE):
+        assert B.workspace_bytes(d, st) == 0
+    assert B.workspace_bytes(good_desc(E=0), B.STAGE_DISPATCH) == 0
+
+
+def test_entry_points_reject_before_launch(lib):
+    d = good_desc()
+    bd = ctypes.byref(d)
+    z = None
+    # route
+    assert lib.brownout_moe_route(bd, z, FAKE, z, z, FAKE, FAKE, FAKE, FAKE, FAKE, z, z) == NULL
+    assert lib.brownout_moe_route(bd, FAKE, FAKE, z, z, z, FAKE, FAKE, FAKE, FAKE, z, z) == NULL
+    assert lib.brownout_moe_route(bd, MISALIGNED, FAKE, z, z, FAKE, FAKE, FAKE, FAKE, FAKE, z, z) == ALIGN
+    bad = ctypes.byref(good_desc(top_k=0))
+    assert lib.brownout_moe_route(bad, FAKE, FAKE, z, z, FAKE, FAKE, FAKE, FAKE, FAKE, z, z) == SHAPE
+    # dispatch
+    need = B.workspace_bytes(d, B.STAGE_DISPATCH)
+    assert lib.brownout_moe_dispatch(bd, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, need, z) == WS
+    assert lib.brownout_moe_dispatch(bd, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, z) == WS
+    assert lib.brownout_moe_dispatch(bd, FAKE, MISALIGNED, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == ALIGN
+    assert lib.brownout_moe_dispatch(bd, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                     ctypes.c_void_p(0x10010), need, z) == ALIGN
+    assert lib.brownout_moe_dispatch(bd, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == NULL
+    # ffn (and its halves)
+    assert lib.brownout_moe_ffn(9, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == UNSUP
+    assert lib.brownout_moe_ffn(1, 0, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert lib.brownout_moe_ffn(1, 257, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert lib.brownout_moe_ffn(1, 4, 128, 250, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert lib.brownout_moe_ffn(1, 4, 128, 256, 512, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == NULL
+    assert lib.brownout_moe_ffn(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
+    assert lib.brownout_moe_ffn_gate_up(1, 4, 128, 256, 512, FAKE, z, FAKE, FAKE, FAKE, z) == NULL
+    assert lib.brownout_moe_ffn_down(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, MISALIGNED, z) == ALIGN
+    # combine
+    assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, z, z, z) == NULL
+    assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
+
+
+def test_zero_tokens_needs_no_pointers(lib):
+    d = good_desc(T=0)
+    bd = ctypes.byref(d)
+    z = None
+    assert lib.brownout_moe_route(bd, z, z, z, z, z, z, z, z, z, z, z) == OK
+    assert lib.brownout_moe_dispatch(bd, z, z, z, z, z, z, z, z, 0, z) == OK
+    assert lib.brownout_moe_combine(bd, z, z, z, z, z, z) == OK
+    assert lib.brownout_moe_ffn(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z) == OK
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    d = good_desc()
+    with pytest.raises(ValueError):
+        B.route(d, torch.zeros(64, 256), torch.zeros(8, 256), None, torch.zeros(8, dtype=torch.int32))
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    monkeypatch.setattr(B, "_lib", None)
+    with pytest.raises(RuntimeError):
+        B.load_library(str(tmp_path / "nope.so"))

@@ -1,0 +1,373 @@
+"""HIP path against the CPU oracle, through the C ABI (needs an MI355X).
+
+Each stage is first fed the oracle's own upstream outputs, so a failure names
+one stage; then the whole layer runs end to end. Small cases (the oracle runs
+them in seconds) span several route/dispatch/FFN tiles and end in ragged
+tails; the full-size workloads are checked in full on every integer output
+and on a sample of tokens (including the first and last row of every group)
+for the float outputs, since each token's output depends on that token only.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (TOL, assert_close_rows, assert_gates, desc_of, dev_tensor, device_weights,
+                      group_boundary_tokens, host_f32, to_storage)
+from paper_2607_04164_amd import binding as B
+from paper_2607_04164_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    "tiny": W.CONFIGS["tiny"],
+    "mixtral-s": W.CONFIGS["mixtral"].with_(name="mixtral-s", T=300, d=512, d_ff=640),
+    "fine-s": W.CONFIGS["fine"].with_(name="fine-s", T=517, d=256, d_ff=384),
+    "heavy-s": W.CONFIGS["heavy"].with_(name="heavy-s", T=700, d=512, d_ff=192, d_ff_shared_each=192),
+    "decode": W.CONFIGS["decode"],
+    "tail": W.LayerConfig("tail", T=33, d=264, E=12, top_k=3, G=5, d_ff=520, dtype="bf16", zipf_s=1.2),
+}
+CASES = [(n, 0) for n in SMALL] + [("tiny", 1), ("tiny", 2), ("fine-s", 1)]
+IDS = [f"{n}-seed{s}" for n, s in CASES]
+
+
+@functools.lru_cache(maxsize=None)
+def case(name, seed):
+    cfg = SMALL[name]
+    L = W.make_layer(cfg, seed)
+    ref = oracle.layer(L, want_intermediates=True)
+    return L, ref
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+
+
+# ---------------------------------------------------------------------------
+# route
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_route_logits_in_exact(name, seed):
+    """Selection, softmax, map and merge on given fp32 logits: integers exact."""
+    L, ref = case(name, seed)
+    cfg = L.cfg
+    z32 = ref["logits"].astype(np.float32)
+    want = oracle.route_from_logits(z32, L.e2g, cfg.top_k, cfg.norm_topk)
+    e2g = torch.from_numpy(L.e2g).cuda()
+    got = B.route(desc_of(cfg), None, None, None, e2g, logits_in=torch.from_numpy(z32).cuda())
+    torch.cuda.synchronize()
+    for k in ("topk_idx", "slot_group"):
+        assert np.array_equal(got[k].cpu().numpy(), want[k]), k
+    assert_gates(got["topk_w"].cpu().numpy(), want["topk_w"], "topk_w")
+    assert_gates(got["slot_gate"].cpu().numpy(), want["slot_gate"], "slot_gate")
+
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_route_exact(name, seed):
+    """Logits computed on the GPU (MFMA for bf16): integers exact against float64 selection."""
+    L, ref = case(name, seed)
+    cfg = L.cfg
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    got = B.route(desc_of(cfg), x, w["w_router"], w["bias"], w["e2g"], want_logits=True)
+    torch.cuda.synchronize()
+    zerr = np.abs(got["logits"].cpu().numpy().astype(np.float64) - ref["logits"]).max()
+    # premise of the float64 recheck: fast logits are far closer than the gap
+    assert zerr < B.ROUTE_RECHECK_GAP / 4, f"fp32 logit error {zerr:.3e}"
+    for k in ("topk_idx", "slot_group"):
+        assert np.array_equal(got[k].cpu().numpy(), ref[k]), k
+    assert_gates(got["topk_w"].cpu().numpy(), ref["topk_w"], "topk_w")
+    assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
+
+
+def test_route_near_ties_decided_in_f64():
+    """Two experts whose logits differ by far less than the fp32 rounding error
+    (and exact ties) are still ordered as float64 orders them."""
+    cfg = W.LayerConfig("ties", T=96, d=256, E=16, top_k=4, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
+    L = W.make_layer(cfg, 5)
+    # expert 7's router row equals expert 3's except one bf16 ulp in column 17;
+    # column 17 of x is tiny, so the two logits differ by |x[t,17]| * ulp
+    wr = L.w_router.copy()
+    wr[7] = wr[3]
+    wr[7, 17] = wr[3, 17] + 1
+    L.w_router = wr
+    x = W.bf16_bits_to_f32(L.x).copy()
+    signs = np.where(np.arange(cfg.T) % 2 == 0, 1.0, -1.0)
+    x[:, 17] = signs * 2.0 ** -(8 + np.arange(cfg.T) % 8)
+    x[::12, 17] = 0.0  # exact ties: lower expert index first
+    L.x = W.f32_to_bf16_bits(x.astype(np.float32))
+    L.bias = L.bias.copy()
+    L.bias[7] = L.bias[3] = np.float32(0.5)
+    ref = oracle.route(L.f32("x"), L.f32("w_router"), L.bias, L.e2g, cfg.top_k)
+    d37 = np.abs(ref["logits"][:, 3] - ref["logits"][:, 7])
+    assert d37.max() < 1e-5 and (d37 == 0).any()
+    w = device_weights(L)
+    got = B.route(desc_of(cfg), dev_tensor(L.x, "bf16"), w["w_router"], w["bias"], w["e2g"])
+    torch.cuda.synchronize()
+    assert np.array_equal(got["topk_idx"].cpu().numpy(), ref["topk_idx"])
+    assert np.array_equal(got["slot_group"].cpu().numpy(), ref["slot_group"])
+    assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
+
+
+# ---------------------------------------------------------------------------
+# dispatch
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_dispatch_exact(name, seed):
+    L, ref = case(name, seed)
+    cfg = L.cfg
+    desc = desc_of(cfg)
+    sg = torch.from_numpy(ref["slot_group"]).cuda()
+    x = dev_tensor(L.x, cfg.dtype)
+    ws = B.new_dispatch_workspace(desc, "cuda")
+    got = B.dispatch(desc, sg, x, ws)
+    torch.cuda.synchronize()
+    N = ref["N"]
+    assert np.array_equal(got["counts"].cpu().numpy(), ref["counts"])
+    assert np.array_equal(got["offsets"].cpu().numpy(), ref["offsets"])
+    assert np.array_equal(got["perm_token"][:N].cpu().numpy(), ref["perm_token"])
+    assert np.array_equal(got["slot_row"].cpu().numpy(), ref["slot_row"])
+    xp = got["x_perm"][:N]
+    want = x[torch.from_numpy(ref["perm_token"]).long().cuda()]
+    assert torch.equal(xp.view(torch.int16) if cfg.dtype == "bf16" else xp.view(torch.int32),
+                       want.view(torch.int16) if cfg.dtype == "bf16" else want.view(torch.int32))
+    assert int(ws.count_nonzero()) == 0, "dispatch must leave its workspace all zero"
+
+
+def test_dispatch_many_tiles_and_reuse():
+    """Several calls in a row on one workspace, T spanning many 256-token tiles."""
+    r = np.random.default_rng(3)
+    for T, k, G in ((5000, 6, 16), (777, 2, 4), (256, 4, 15), (1, 1, 1), (4097, 8, 64)):
+        sg = r.integers(-1, G, size=(T, k)).astype(np.int32)
+        for t in range(T):  # at most one valid slot per group per token, as route guarantees
+            seen = set()
+            for i in range(k):
+                if sg[t, i] in seen:
+                    sg[t, i] = -1
+                elif sg[t, i] >= 0:
+                    seen.add(sg[t, i])
+        ref = oracle.dispatch(sg, G)
+        desc = B.make_desc(T, 64, max(G, k), k, G, 64)
+        x = torch.randn(T, 64, device="cuda").to(torch.bfloat16)
+        ws = B.new_dispatch_workspace(B.make_desc(5000, 64, 64, 8, 64, 64), "cuda")
+        for _ in range(2):
+            got = B.dispatch(desc, torch.from_numpy(sg).cuda(), x, ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(got["offsets"].cpu().numpy(), ref["offsets"])
+            assert np.array_equal(got["slot_row"].cpu().numpy(), ref["slot_row"])
+            assert np.array_equal(got["perm_token"][:ref["N"]].cpu().numpy(), ref["perm_token"])
+        assert int(ws.count_nonzero()) == 0
+
+
+# ---------------------------------------------------------------------------
+# ffn
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_ffn(name, seed):
+    L, ref = case(name, seed)
+    cfg = L.cfg
+    N, cap = ref["N"], cfg.T * cfg.top_k
+    w = device_weights(L)
+    a = torch.full((cap, cfg.d), 7.0, device="cuda", dtype=torch.bfloat16 if cfg.dtype == "bf16" else torch.float32)
+    a[:N] = dev_tensor(to_storage(ref["x_perm"], cfg.dtype), cfg.dtype)
+    sentinel = -3.0
+    y = torch.full_like(a, sentinel)
+    offs = torch.from_numpy(ref["offsets"]).cuda()
+    yg, hg = B.ffn(offs, a, w["w_gate"], w["w_up"], w["w_down"], y=y)
+    torch.cuda.synchronize()
+    assert_close_rows(host_f32(hg[:N]), ref["h"], cfg.dtype, "h")
+    assert_close_rows(host_f32(yg[:N]), ref["y"], cfg.dtype, "y")
+    assert bool((yg[N:] == sentinel).all()), "rows past offsets[G] must not be written"
+    if cfg.n_shared:
+        xs = dev_tensor(L.x, cfg.dtype)
+        ys, _ = B.ffn(torch.tensor([0, cfg.T], dtype=torch.int32, device="cuda"), xs, w["w_gate_sh"],
+                      w["w_up_sh"], w["w_down_sh"])
+        torch.cuda.synchronize()
+        assert_close_rows(host_f32(ys), ref["y_shared"], cfg.dtype, "y_shared")
+
+
+def test_ffn_skewed_and_empty_segments():
+    """Hot/cold segment sizes (1 row .. many tiles) and empty segments anywhere."""
+    r = np.random.default_rng(11)
+    d, f, nseg = 256, 200, 7
+    sizes = [0, 1, 300, 0, 129, 2, 0]
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N = int(offsets[-1])
+    a = W.f32_to_bf16_bits(r.standard_normal((N + 5, d)).astype(np.float32))
+    wg = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / 16).astype(np.float32))
+    wu = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / 16).astype(np.float32))
+    wd = W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / 16).astype(np.float32))
+    ref_y = oracle.ffn(offsets, W.bf16_bits_to_f32(a), *(W.bf16_bits_to_f32(t) for t in (wg, wu, wd)))
+    yg, _ = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
+                  dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"))
+    torch.cuda.synchronize()
+    assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
+
+
+# ---------------------------------------------------------------------------
+# combine
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_combine(name, seed):
+    L, ref = case(name, seed)
+    cfg = L.cfg
+    cap = cfg.T * cfg.top_k
+    y_store = to_storage(ref["y"], cfg.dtype)
+    y = torch.zeros((cap, cfg.d), device="cuda", dtype=torch.bfloat16 if cfg.dtype == "bf16" else torch.float32)
+    y[:ref["N"]] = dev_tensor(y_store, cfg.dtype)
+    ysh_np = ysh = None
+    if cfg.n_shared:
+        ysh_np = to_storage(ref["y_shared"], cfg.dtype)
+        ysh = dev_tensor(ysh_np, cfg.dtype)
+    out = B.combine(desc_of(cfg), torch.from_numpy(ref["slot_row"]).cuda(),
+                    torch.from_numpy(ref["slot_gate"]).cuda(), y, ysh)
+    torch.cuda.synchronize()
+    widen = (lambda a: W.bf16_bits_to_f32(a)) if cfg.dtype == "bf16" else (lambda a: a)
+    want = oracle.combine(ref["slot_row"], ref["slot_gate"], widen(y_store),
+                          None if ysh_np is None else widen(ysh_np), d=cfg.d)
+    assert_close_rows(host_f32(out), want, cfg.dtype, "out")
+
+
+# ---------------------------------------------------------------------------
+# whole layer
+
+def run_layer(L):
+    cfg = L.cfg
+    layer = B.LayerForward(desc_of(cfg), device_weights(L))
+    out = layer(dev_tensor(L.x, cfg.dtype))
+    torch.cuda.synchronize()
+    return layer, out
+
+
+def check_layer(L, ref, layer, out):
+    cfg = L.cfg
+    r, dsp = layer.bufs["route"], layer.bufs["dispatch"]
+    for k in ("topk_idx", "slot_group"):
+        assert np.array_equal(r[k].cpu().numpy(), ref[k]), k
+    for k in ("counts", "offsets", "slot_row"):
+        assert np.array_equal(dsp[k].cpu().numpy(), ref[k]), k
+    assert np.array_equal(dsp["perm_token"][:ref["N"]].cpu().numpy(), ref["perm_token"])
+    assert_gates(r["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
+    assert_close_rows(host_f32(out), ref["out"], cfg.dtype, "out")
+
+
+@pytest.mark.parametrize("name,seed", CASES, ids=IDS)
+def test_layer_end_to_end(name, seed):
+    L, ref = case(name, seed)
+    layer, out = run_layer(L)
+    check_layer(L, ref, layer, out)
+
+
+EDGE = {
+    "T1": W.LayerConfig("T1", T=1, d=128, E=8, top_k=2, G=4, d_ff=64, dtype="bf16", zipf_s=1.0),
+    "k1": W.LayerConfig("k1", T=200, d=128, E=8, top_k=1, G=4, d_ff=96, dtype="bf16", zipf_s=1.0),
+    "G1": W.LayerConfig("G1", T=150, d=128, E=16, top_k=4, G=1, d_ff=96, dtype="bf16", zipf_s=1.0),
+    "identity": W.LayerConfig("identity", T=150, d=128, E=8, top_k=2, G=8, d_ff=96, dtype="bf16", zipf_s=1.0),
+    "E1": W.LayerConfig("E1", T=70, d=64, E=1, top_k=1, G=1, d_ff=64, dtype="bf16", zipf_s=1.0),
+    "maxE": W.LayerConfig("maxE", T=90, d=128, E=256, top_k=16, G=64, d_ff=64, dtype="bf16", zipf_s=1.1),
+    "E100": W.LayerConfig("E100", T=300, d=192, E=100, top_k=5, G=20, d_ff=72, dtype="bf16", zipf_s=1.2),
+    "k_eq_E": W.LayerConfig("k_eq_E", T=64, d=64, E=4, top_k=4, G=2, d_ff=64, dtype="bf16", zipf_s=1.0),
+    "f32-tail": W.LayerConfig("f32-tail", T=45, d=72, E=10, top_k=3, G=4, d_ff=40, dtype="f32",
+                              zipf_s=1.2, router_std=0.3, norm_topk=1),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_layer_edge_shapes(name):
+    cfg = EDGE[name]
+    L = W.make_layer(cfg, 0)
+    if name == "identity":
+        L.e2g = np.arange(cfg.E, dtype=np.int32)
+    ref = oracle.layer(L, want_intermediates=True)
+    layer, out = run_layer(L)
+    check_layer(L, ref, layer, out)
+
+
+def test_layer_empty_groups_in_map():
+    """Groups no expert maps to (first, middle and last) are legal and stay empty."""
+    cfg = W.LayerConfig("holes", T=260, d=128, E=8, top_k=3, G=7, d_ff=64, dtype="bf16", zipf_s=1.0)
+    L = W.make_layer(cfg, 2)
+    L.e2g = np.array([1, 1, 2, 2, 4, 4, 5, 5], np.int32)
+    ref = oracle.layer(L, want_intermediates=True)
+    assert ref["counts"][0] == ref["counts"][3] == ref["counts"][6] == 0
+    layer, out = run_layer(L)
+    check_layer(L, ref, layer, out)
+
+
+def test_zero_tokens_is_noop():
+    cfg = W.LayerConfig("T0", T=0, d=64, E=8, top_k=2, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
+    desc = desc_of(cfg)
+    e = torch.zeros(8, dtype=torch.int32, device="cuda")
+    x = torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda")
+    wr = torch.zeros((8, 64), dtype=torch.bfloat16, device="cuda")
+    out = B.route(desc, x, wr, None, e)
+    assert out["topk_idx"].shape == (0, 2)
+
+
+def test_deterministic_bits():
+    L, _ = case("heavy-s", 0)
+    _, a = run_layer(L)
+    _, b = run_layer(L)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_token_order_invariance():
+    """Permuting tokens permutes the output rows bit for bit and keeps the counts."""
+    L, _ = case("fine-s", 0)
+    perm = np.random.default_rng(9).permutation(L.cfg.T)
+    la, a = run_layer(L)
+    L2 = dataclasses.replace(L, x=L.x[perm].copy())
+    lb, b = run_layer(L2)
+    assert torch.equal(b.view(torch.int16), a[torch.from_numpy(perm).long().cuda()].view(torch.int16))
+    assert torch.equal(la.bufs["dispatch"]["counts"], lb.bufs["dispatch"]["counts"])
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads: integers in full, floats on sampled tokens
+
+@functools.lru_cache(maxsize=1)
+def full_case(name):
+    cfg = W.CONFIGS[name]
+    L = W.make_layer(cfg, 0)
+    return L
+
+
+@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral"])
+def test_full_size_sampled(name):
+    L = full_case(name)
+    cfg = L.cfg
+    layer, out = run_layer(L)
+    # integer outputs in full
+    r = oracle.route(L.f32("x"), L.f32("w_router"), L.bias, L.e2g, cfg.top_k, cfg.norm_topk)
+    dsp = oracle.dispatch(r["slot_group"], cfg.G)
+    gr, gd = layer.bufs["route"], layer.bufs["dispatch"]
+    assert np.array_equal(gr["topk_idx"].cpu().numpy(), r["topk_idx"])
+    assert np.array_equal(gr["slot_group"].cpu().numpy(), r["slot_group"])
+    assert_gates(gr["slot_gate"].cpu().numpy(), r["slot_gate"], "slot_gate")
+    for k in ("counts", "offsets", "slot_row"):
+        assert np.array_equal(gd[k].cpu().numpy(), dsp[k]), k
+    assert np.array_equal(gd["perm_token"][:dsp["N"]].cpu().numpy(), dsp["perm_token"])
+    # float outputs on a token sample: group boundary rows plus random tokens
+    rng = np.random.default_rng(1)
+    extra = 8 if name == "mixtral" else 32
+    sample = np.unique(np.concatenate([group_boundary_tokens(dsp["perm_token"], dsp["offsets"]),
+                                       rng.choice(cfg.T, size=min(extra, cfg.T), replace=False),
+                                       [0, cfg.T - 1]]))
+    sub = dataclasses.replace(L, cfg=cfg.with_(T=len(sample)), x=L.x[sample].copy())
+    ref = oracle.layer(sub, want_intermediates=True)
+    assert np.array_equal(ref["topk_idx"], r["topk_idx"][sample])
+    assert_close_rows(host_f32(out[torch.from_numpy(sample).cuda()]), ref["out"], cfg.dtype, "out")
+    # united-expert outputs of the sampled tokens' rows
+    sr = gd["slot_row"].cpu().numpy()[sample]
+    rows = sr[sr >= 0]
+    ref_rows = ref["slot_row"][sr >= 0]
+    assert_close_rows(host_f32(layer.bufs["y"][torch.from_numpy(rows).long().cuda()]),
+                      ref["y"][ref_rows], cfg.dtype, "y_perm")
