@@ -30,6 +30,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+typedef float f32x2_hw __attribute__((ext_vector_type(2)));
+
+// two floats -> packed bf16 (low, high) with the hardware round-to-nearest-even convert
+__device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi) {
+    f32x2_hw v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_hw));
+}
+
+// silu(g) * u = g / (1 + e^-g) * u with the hardware exp2 and reciprocal
+// (relative error ~1e-7, far below the bf16 rounding that follows)
+__device__ __forceinline__ float silu_mul(float g, float u) {
+    return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)) * u;
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8, v);
 }

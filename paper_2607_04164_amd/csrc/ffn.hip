@@ -108,7 +108,31 @@ __device__ __forceinline__ void gemm_sstore(const uint4 (&ra)[C::A_CH], const ui
         }
 }
 
-template <bool GATED, int BM, int BN, int BK>
+template <class C>
+__device__ __forceinline__ void gemm_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB],
+                                           const uint16_t* a_base, const uint16_t* b_base, int kk) {
+    constexpr int BN = C::B_CH * kGemmThreads / C::KCH;
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb) af[mb] = *(const uint4*)(a_base + mb * 32 * C::LROW + kk * 16);
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb)
+            bf[mat][nb] = *(const uint4*)(b_base + (size_t)(mat * 2 * BN + nb * 32) * C::LROW + kk * 16);
+}
+
+template <class C>
+__device__ __forceinline__ void gemm_mfmas(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                           const uint4 (&bf)[C::NMAT][C::NB]) {
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+}
+
+template <bool GATED, int BM, int BN, int BK, bool FDB>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_kernel(GemmParams p) {
     using C = GemmCfg<GATED, BM, BN, BK>;
     __shared__ __align__(16) char smem[C::SMEM];
@@ -179,26 +203,26 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_kernel(GemmParam
         const bool more = kt + 1 < nk;
         if (more) gemm_gload<C>(ra, rb, p.A, Bm[0], Bm[1], tid, (kt + 1) * BK, m0, m_end, n0, N, K);
         const uint16_t* a_base = sA + (size_t)(buf * BM + wm * C::WTM + l32) * C::LROW + hi8;
+        const uint16_t* b_base = sB + (size_t)(buf * BN + wn * C::WTN + l32) * C::LROW + hi8;
+        if constexpr (FDB) {
+            // fragments of sub-step kk+1 are read from LDS while sub-step kk runs on the MFMA pipe
+            uint4 af[2][C::MB];
+            uint4 bf[2][C::NMAT][C::NB];
+            gemm_frags<C>(af[0], bf[0], a_base, b_base, 0);
 #pragma unroll
-        for (int kk = 0; kk < BK / 16; ++kk) {
-            uint4 af[C::MB];
-            uint4 bf[C::NMAT][C::NB];
+            for (int kk = 0; kk < BK / 16; ++kk) {
+                const int cur = kk & 1;
+                if (kk + 1 < BK / 16) gemm_frags<C>(af[cur ^ 1], bf[cur ^ 1], a_base, b_base, kk + 1);
+                gemm_mfmas<C>(acc, af[cur], bf[cur]);
+            }
+        } else {
 #pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb)
-                af[mb] = *(const uint4*)(a_base + mb * 32 * C::LROW + kk * 16);
-#pragma unroll
-            for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-                for (int nb = 0; nb < C::NB; ++nb)
-                    bf[mat][nb] = *(const uint4*)(sB +
-                        (size_t)((mat * 2 + buf) * BN + wn * C::WTN + nb * 32 + l32) * C::LROW + hi8 + kk * 16);
-#pragma unroll
-            for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < C::NB; ++nb)
-                        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+            for (int kk = 0; kk < BK / 16; ++kk) {
+                uint4 af[C::MB];
+                uint4 bf[C::NMAT][C::NB];
+                gemm_frags<C>(af, bf, a_base, b_base, kk);
+                gemm_mfmas<C>(acc, af, bf);
+            }
         }
         if (more) gemm_sstore<C>(ra, rb, sA, sB, tid, buf ^ 1);
         __syncthreads();
@@ -235,15 +259,315 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_kernel(GemmParam
     }
 }
 
-template <bool GATED, int BM, int BN, int BK>
+template <bool GATED, int BM, int BN, int BK, bool FDB>
 hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
     const int64_t mt_max = ceil_div64(g.rows_cap, BM) + g.n_seg;
     const int64_t nt = ceil_div64(g.N, BN);
     int64_t blocks = mt_max * nt;
     blocks = (blocks + 7) / 8 * 8;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((grouped_gemm_kernel<GATED, BM, BN, BK>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((grouped_gemm_kernel<GATED, BM, BN, BK, FDB>), dim3((unsigned)blocks),
                        dim3(kGemmThreads), 0, s, g);
+    return hipGetLastError();
+}
+
+// ---- bf16 grouped GEMM with direct global->LDS loads (K % BK == 0)
+//
+// 256 x 256 workgroup tile (gate/up: 128 columns of each matrix), 128 x 128
+// per wave, a ring of LDS stages filled by global_load_lds_dwordx4 (no
+// staging registers, no LDS store instructions). A stage holds every tile
+// row's BK k-values as one LDS row of BK*2 bytes whose 16-byte chunks are
+// XOR-swizzled by (row >> 1), so the 32 rows of an MFMA fragment read without
+// bank conflicts; one DMA instruction fills 64/(BK/8) consecutive rows, each
+// lane fetching the global chunk that belongs in its LDS slot (the lanes of a
+// row read the row's contiguous bytes). The DMA and the barrier are issued
+// through inline asm: with the builtin, the compiler would wait for every
+// outstanding DMA before each LDS read and at each barrier, defeating the ring.
+// Per K-step: read the fragments of sub-step 1, run sub-step 0 on the MFMA
+// pipe, wait for this wave's DMAs of the next stage, barrier (after it every
+// wave has finished reading this stage and the next stage is resident), issue
+// the DMAs four stages ahead into this stage's slot, read the next stage's
+// sub-step-0 fragments, run sub-step 1.
+
+// K-step and ring depth of the DMA kernels. BK = 64 makes every DMA row a
+// full 128-byte line (8 rows per instruction), which the L2 and MALL serve
+// faster than 64-byte pieces; two 64 KB stages leave one stage in flight.
+// Measured on the grouped workloads, more stages of BK = 32 did not help:
+// the pipeline is bound by L2/MALL throughput, not by latency.
+#ifdef BMOE_FORCE_DMA_BK
+constexpr int kDmaBK = BMOE_FORCE_DMA_BK;
+#else
+constexpr int kDmaBK = 64;
+#endif
+#ifdef BMOE_FORCE_DMA_STAGES
+constexpr int kDmaStages = BMOE_FORCE_DMA_STAGES;
+#else
+constexpr int kDmaStages = 2;
+#endif
+
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr)
+                 : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+template <int PER>
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+    constexpr int kMax = 63;  // largest vmcnt the instruction encodes
+    if (n >= 4) wait_vmcnt<(4 * PER > kMax ? kMax : 4 * PER)>();
+    else if (n == 3) wait_vmcnt<(3 * PER > kMax ? kMax : 3 * PER)>();
+    else if (n == 2) wait_vmcnt<(2 * PER > kMax ? kMax : 2 * PER)>();
+    else if (n == 1) wait_vmcnt<PER>();
+    else wait_vmcnt<0>();
+}
+__device__ __forceinline__ void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <bool GATED, int NSTAGE, int BKV>
+struct DmaCfg {
+    static constexpr int BM = 256, BK = BKV, STAGES = NSTAGE, KC = BK / 8;  // KC: 16-byte chunks per row
+    static constexpr int SUB = BK / 16;                                      // MFMA sub-steps per stage
+    static constexpr int BN = GATED ? 128 : 256;  // output columns per matrix
+    static constexpr int NMAT = GATED ? 2 : 1;
+    static constexpr int RB = NMAT * BN;          // B rows staged per K-step (256)
+    static constexpr int WTM = BM / 2, WTN = BN / 2;
+    static constexpr int MB = WTM / 32, NB = WTN / 32;
+    static constexpr int ROW_BYTES = BK * 2;
+    static constexpr int ROWS_PER_DMA = 64 / KC;                   // rows one DMA instruction fills
+    static constexpr int A_DMA = BM / (4 * ROWS_PER_DMA);          // per wave per stage
+    static constexpr int B_DMA = RB / (4 * ROWS_PER_DMA);
+    static constexpr int DMA_PER_STAGE = A_DMA + B_DMA;
+    static constexpr int A_STAGE = BM * ROW_BYTES, B_STAGE = RB * ROW_BYTES;
+    static constexpr int STAGE = A_STAGE + B_STAGE;
+    static constexpr int SROW = WTN + 8;
+    static constexpr int EPI = 4 * WTM * SROW * 2;
+    static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;  // tile-schedule arrays
+    static constexpr int RING = STAGES * STAGE;
+    static constexpr int SMEM = (RING > EPI ? RING : EPI) > SCHED ? (RING > EPI ? RING : EPI) : SCHED;
+    static_assert((KC == 4 || KC == 8) && BM == 256 && RB == 256, "tile shape");
+    static_assert(SUB % 2 == 0, "fragment double buffer alternates within a stage");
+    static_assert(SMEM <= 160 * 1024, "LDS of one workgroup");
+};
+
+// 16-byte chunk swizzle of a tile row: conflict-free 128-bit fragment reads
+template <int KC>
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & (KC - 1); }
+
+// LDS byte offset of logical 16-byte chunk c of tile row r within a stage region
+template <class C>
+__device__ __forceinline__ int lds_off(int r, int c) { return r * C::ROW_BYTES + ((c ^ swz<C::KC>(r)) << 4); }
+
+template <class C>
+__device__ __forceinline__ void dma_stage(const uint16_t* const (&a_src)[C::A_DMA],
+                                          const uint16_t* const (&b_src)[C::B_DMA], uint32_t stage_lds,
+                                          int wave, int k0) {
+    // instruction i of wave w fills ROWS_PER_DMA consecutive rows (1 KB of LDS)
+#pragma unroll
+    for (int i = 0; i < C::A_DMA; ++i)
+        dma16(a_src[i] + k0, __builtin_amdgcn_readfirstlane(
+                                 stage_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES));
+#pragma unroll
+    for (int i = 0; i < C::B_DMA; ++i)
+        dma16(b_src[i] + k0, __builtin_amdgcn_readfirstlane(
+                                 stage_lds + C::A_STAGE + ((wave * C::B_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES));
+}
+
+template <class C>
+__device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB], const char* stage,
+                                          int wm, int wn, int lane, int kk) {
+    const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb)
+        af[mb] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + mb * 32 + l32, c));
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb)
+            bf[mat][nb] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
+}
+
+template <class C>
+__device__ __forceinline__ void dma_mfmas(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                          const uint4 (&bf)[C::NMAT][C::NB]) {
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+}
+
+template <bool GATED, int NSTAGE, int BKV>
+__global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmParams p) {
+    using C = DmaCfg<GATED, NSTAGE, BKV>;
+    constexpr int BM = C::BM, BN = C::BN;
+    __shared__ __align__(16) char smem[C::SMEM];
+    // the tile-schedule arrays live in the first bytes of the ring; they are
+    // dead (copied to registers, then a barrier) before the first DMA
+    int* s_scan = (int*)smem;
+    int* s_mt = s_scan + 256;
+    int* s_beg = s_mt + BMOE_MAX_EXPERTS + 1;
+    int* s_end = s_beg + BMOE_MAX_EXPERTS;
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n_seg = p.n_seg, N = p.N, K = p.K;
+
+    // ---- tile schedule from the device offsets (same mapping as the other GEMMs)
+    int cnt = 0;
+    if (tid < n_seg) {
+        int beg = min(max(p.offsets[tid], 0), p.rows_cap);
+        int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
+        s_beg[tid] = beg;
+        s_end[tid] = end;
+        cnt = ceil_div(end - beg, BM);
+    }
+    int total_mt;
+    const int ex = block_exclusive_scan_256(cnt, s_scan, &total_mt);
+    if (tid < n_seg) s_mt[tid] = ex;
+    if (tid == 0) s_mt[n_seg] = total_mt;
+    __syncthreads();
+    const int NT = ceil_div(N, BN);
+    const int L = xcd_swizzle(blockIdx.x, gridDim.x);
+    if (L >= total_mt * NT) return;
+    int lo = 0, hi = n_seg - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_mt[mid] * NT <= L) lo = mid;
+        else hi = mid - 1;
+    }
+    const int s = lo;
+    const int mts = s_mt[s + 1] - s_mt[s];
+    const int local = L - s_mt[s] * NT;
+    const int nt = local / mts, mt = local % mts;
+    const int m0 = s_beg[s] + mt * BM, m_end = s_end[s];
+    const int n0 = nt * BN;
+    __syncthreads();  // schedule arrays are overwritten by the first DMAs
+
+    // ---- per-lane DMA sources: lane l of instruction i of wave w fills LDS row
+    // r = (w*N_DMA + i)*ROWS_PER_DMA + l/KC, physical chunk l%KC, i.e. logical
+    // chunk (l%KC) ^ swz(r); the KC lanes of a row read its contiguous bytes
+    const uint16_t* a_src[C::A_DMA];
+    const uint16_t* b_src[C::B_DMA];
+    const int lrow = lane / C::KC, lchk = lane % C::KC;
+#pragma unroll
+    for (int i = 0; i < C::A_DMA; ++i) {
+        const int r = (wave * C::A_DMA + i) * C::ROWS_PER_DMA + lrow;
+        const int row = min(m0 + r, m_end - 1);
+        a_src[i] = p.A + (size_t)row * K + ((lchk ^ swz<C::KC>(r)) << 3);
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_DMA; ++i) {
+        const int r = (wave * C::B_DMA + i) * C::ROWS_PER_DMA + lrow;
+        const int mat = GATED ? r / BN : 0;
+        const int n = min(n0 + r % BN, N - 1);
+        b_src[i] = (mat ? p.B1 : p.B0) + ((size_t)s * N + n) * K + ((lchk ^ swz<C::KC>(r)) << 3);
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nk = K / C::BK;
+
+    f32x16 acc[C::NMAT][C::MB][C::NB];
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc[mat][mb][nb][i] = 0.f;
+
+    // ---- prologue: the first STAGES stages in flight, wait for stage 0
+#pragma unroll
+    for (int st = 0; st < C::STAGES; ++st)
+        if (st < nk) dma_stage<C>(a_src, b_src, lds0 + st * C::STAGE, wave, st * C::BK);
+    wait_vmcnt_rt<C::DMA_PER_STAGE>(min(nk, C::STAGES) - 1);
+    wg_barrier();
+    uint4 af0[C::MB], af1[C::MB];
+    uint4 bf0[C::NMAT][C::NB], bf1[C::NMAT][C::NB];
+    dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
+
+    // The LDS reads of every K-step are unconditional (the last step reads a
+    // stale slot and drops it), so the compiler's LDS wait counts never merge
+    // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
+    // sched_barrier(0) fences keep each group of fragment reads ahead of the
+    // MFMA group that hides its latency (the scheduler would otherwise sink
+    // the next stage's reads to the top of the next iteration).
+    int slot = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
+        const char* stage = smem + slot * C::STAGE;
+#pragma unroll
+        for (int j = 0; j < C::SUB; ++j) {
+            uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
+            uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
+            uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
+            uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
+            if (j + 1 < C::SUB) dma_frags<C>(ga, gb, stage, wm, wn, lane, j + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            dma_mfmas<C>(acc, fa, fb);
+            __builtin_amdgcn_sched_barrier(0);
+            if (j == C::SUB - 2) {
+                // stages issued so far: 0 .. min(nk-1, kt+STAGES-1); stage kt+1 must be resident
+                wait_vmcnt_rt<C::DMA_PER_STAGE>(max(0, min(nk - 1, kt + C::STAGES - 1) - (kt + 1)));
+                lds_reads_done();
+                wg_barrier();
+                if (kt + C::STAGES < nk)
+                    dma_stage<C>(a_src, b_src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK);
+                // registers of this sub-step are free now: next stage, sub-step 0
+                dma_frags<C>(fa, fb, smem + next * C::STAGE, wm, wn, lane, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        slot = next;
+    }
+    __syncthreads();
+
+    // ---- epilogue: stage the wave's tile in LDS, then 128-bit row stores
+    uint16_t* st = (uint16_t*)smem + (size_t)wave * C::WTM * C::SROW;
+    const int l32 = lane & 31;
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) {
+                float v0, v1;
+                if constexpr (GATED) {
+                    v0 = silu_mul(acc[0][mb][nb][i], acc[1][mb][nb][i]);
+                    v1 = silu_mul(acc[0][mb][nb][i + 1], acc[1][mb][nb][i + 1]);
+                } else {
+                    v0 = acc[0][mb][nb][i];
+                    v1 = acc[0][mb][nb][i + 1];
+                }
+                const uint32_t pk = pack_bf16x2_hw(v0, v1);
+                const int r = mb * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+                const int c = nb * 32 + l32;
+                st[r * C::SROW + c] = (uint16_t)pk;
+                st[(r + 1) * C::SROW + c] = (uint16_t)(pk >> 16);
+            }
+    __syncthreads();
+    constexpr int CPR = C::WTN / 8;
+    const int row0 = m0 + wm * C::WTM, col0 = n0 + wn * C::WTN;
+#pragma unroll 4
+    for (int c = lane; c < C::WTM * CPR; c += 64) {
+        const int r = c / CPR, cc = c % CPR;
+        const int gm = row0 + r, gn = col0 + cc * 8;
+        if (gm < m_end && gn < N)
+            *(uint4*)(p.C + (size_t)gm * N + gn) = *(const uint4*)(st + r * C::SROW + cc * 8);
+    }
+}
+
+template <bool GATED>
+hipError_t launch_gemm_dma(const GemmParams& g, hipStream_t s) {
+    using C = DmaCfg<GATED, kDmaStages, kDmaBK>;
+    const int64_t mt_max = ceil_div64(g.rows_cap, C::BM) + g.n_seg;
+    const int64_t nt = ceil_div64(g.N, C::BN);
+    int64_t blocks = (mt_max * nt + 7) / 8 * 8;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, kDmaStages, kDmaBK>), dim3((unsigned)blocks), dim3(kGemmThreads), 0,
+                       s, g);
     return hipGetLastError();
 }
 
@@ -299,6 +623,24 @@ __global__ __launch_bounds__(256) void ffn_f32_down_kernel(const float* __restri
 
 }  // namespace
 
+// Workgroup tile of the bf16 grouped GEMMs. 256-row tiles (128x128 per wave)
+// halve the LDS traffic per MFMA but pad each group to a multiple of 256
+// rows, so they are used when groups average well above that.
+enum { kTile128 = 0, kTile256 = 1, kTileDma = 2 };
+#ifdef BMOE_FORCE_FFN_FDB
+constexpr bool kFdb256 = BMOE_FORCE_FFN_FDB;
+#else
+constexpr bool kFdb256 = false;  // no registers left for a second fragment set
+#endif
+static int ffn_tile(const FfnArgs& a) {
+#ifdef BMOE_FORCE_FFN_TILE
+    return BMOE_FORCE_FFN_TILE;
+#else
+    if ((int64_t)a.rows_cap < (int64_t)1024 * a.n_seg) return kTile128;
+    return (a.d % kDmaBK == 0 && a.d_ff % kDmaBK == 0) ? kTileDma : kTile256;
+#endif
+}
+
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (a.rows_cap == 0) return hipSuccess;
     const bool up = part != 2, down = part != 1;
@@ -319,16 +661,21 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
         }
         return hipSuccess;
     }
+    const int tile = ffn_tile(a);
     if (up) {
         GemmParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up,
                       (uint16_t*)a.h, a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
-        hipError_t e = launch_gemm<true, 128, 128, 64>(g1, s);
+        hipError_t e = tile == kTileDma   ? launch_gemm_dma<true>(g1, s)
+                       : tile == kTile256 ? launch_gemm<true, 256, 128, 64, kFdb256>(g1, s)
+                                          : launch_gemm<true, 128, 128, 64, true>(g1, s);
         if (e != hipSuccess) return e;
     }
     if (down) {
         GemmParams g2{(const uint16_t*)a.h, (const uint16_t*)a.w_down, nullptr, (uint16_t*)a.y,
                       a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff};
-        return launch_gemm<false, 128, 256, 64>(g2, s);
+        return tile == kTileDma   ? launch_gemm_dma<false>(g2, s)
+               : tile == kTile256 ? launch_gemm<false, 256, 256, 64, kFdb256>(g2, s)
+                                  : launch_gemm<false, 128, 256, 64, true>(g2, s);
     }
     return hipSuccess;
 }

@@ -212,6 +212,38 @@ def test_ffn_skewed_and_empty_segments():
     assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
 
 
+LARGE_TILE_FFN = [
+    # (segment sizes, rows_cap, d, d_ff): rows_cap >= 1024 * segments selects the
+    # 256-row tiles; d and d_ff multiples of 64 select the direct-to-LDS kernels
+    ((700, 333), 2048, 256, 384),
+    ((1000, 0, 513, 1), 4096, 320, 448),   # N tails in both GEMMs, empty and 1-row segments
+    ((0, 1290), 2048, 512, 192),
+    ((1000, 0, 513, 1), 4096, 288, 352),   # not multiples of 64: register-staged 256-row kernels
+    ((257,), 1024, 264, 200),
+]
+
+
+@pytest.mark.parametrize("sizes,cap,d,f", LARGE_TILE_FFN, ids=[f"seg{len(c[0])}-d{c[2]}-f{c[3]}" for c in LARGE_TILE_FFN])
+def test_ffn_large_tile_paths(sizes, cap, d, f):
+    r = np.random.default_rng(len(sizes) * 1000 + d)
+    nseg = len(sizes)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N = int(offsets[-1])
+    a = W.f32_to_bf16_bits(r.standard_normal((cap, d)).astype(np.float32))
+    wg = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32))
+    wu = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32))
+    wd = W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / np.sqrt(d)).astype(np.float32))
+    ref_y, ref_h = oracle.ffn(offsets, W.bf16_bits_to_f32(a)[:max(N, 1)],
+                              *(W.bf16_bits_to_f32(t) for t in (wg, wu, wd)), want_h=True)
+    y = torch.full((cap, d), -5.0, dtype=torch.bfloat16, device="cuda")
+    yg, hg = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
+                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"), y=y)
+    torch.cuda.synchronize()
+    assert_close_rows(host_f32(hg[:N]), ref_h, "bf16", "h")
+    assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
+    assert bool((yg[N:] == -5.0).all()), "rows past offsets[n_seg] must not be written"
+
+
 # ---------------------------------------------------------------------------
 # combine
 
