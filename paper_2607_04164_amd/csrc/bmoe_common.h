@@ -64,6 +64,39 @@ __device__ __forceinline__ f32x16 mfma32(const uint4& a, const uint4& b, f32x16 
 __host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// ---- direct global->LDS loads and the waits that go with them
+//
+// global_load_lds_dwordx4: every lane copies 16 bytes from its global address
+// to LDS at M0 + 16 * lane. Issued through inline asm because with the
+// builtin the compiler waits for every outstanding copy before each LDS read
+// and at each barrier; callers wait explicitly with wait_vmcnt / wg_barrier.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr)
+                 : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// wait until at most PER*n of this wave's vector-memory operations are in flight (n in 0..7)
+template <int PER>
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+#define BMOE_VMW(m) wait_vmcnt<((m) * PER > 63 ? 63 : (m) * PER)>()
+    switch (n < 0 ? 0 : n) {
+        case 0: BMOE_VMW(0); break;
+        case 1: BMOE_VMW(1); break;
+        case 2: BMOE_VMW(2); break;
+        case 3: BMOE_VMW(3); break;
+        case 4: BMOE_VMW(4); break;
+        case 5: BMOE_VMW(5); break;
+        case 6: BMOE_VMW(6); break;
+        default: BMOE_VMW(7); break;
+    }
+#undef BMOE_VMW
+}
+__device__ __forceinline__ void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // Block-wide exclusive scan of up to 256 ints held one per thread (blockDim = 256).
 // `buf` is 256 ints of LDS. Returns the exclusive prefix; *total gets the sum.
 __device__ __forceinline__ int block_exclusive_scan_256(int v, int* buf, int* total) {

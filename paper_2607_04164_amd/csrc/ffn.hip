@@ -305,25 +305,6 @@ constexpr int kDmaStages = BMOE_FORCE_DMA_STAGES;
 constexpr int kDmaStages = 2;
 #endif
 
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr)
-                 : "memory", "m0");
-}
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-template <int PER>
-__device__ __forceinline__ void wait_vmcnt_rt(int n) {
-    constexpr int kMax = 63;  // largest vmcnt the instruction encodes
-    if (n >= 4) wait_vmcnt<(4 * PER > kMax ? kMax : 4 * PER)>();
-    else if (n == 3) wait_vmcnt<(3 * PER > kMax ? kMax : 3 * PER)>();
-    else if (n == 2) wait_vmcnt<(2 * PER > kMax ? kMax : 2 * PER)>();
-    else if (n == 1) wait_vmcnt<PER>();
-    else wait_vmcnt<0>();
-}
-__device__ __forceinline__ void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <bool GATED, int NSTAGE, int BKV>
 struct DmaCfg {

@@ -3,22 +3,25 @@
 //
 // One workgroup (4 waves) owns BT = 16*TB tokens:
 //   1. logits tile [BT, E] into LDS:
-//        bf16: x rows stream from HBM straight into MFMA A-fragments; W_router
-//              is staged through LDS in super-chunks of KS*64 columns (double
-//              buffered) and shared by the 4 waves; 16x16x32 bf16 MFMA, fp32
-//              accumulate; with KS > 1 the waves split the d axis and their
-//              partial tiles are summed in LDS in a fixed order;
+//        bf16: x rows and W_router rows are copied straight into LDS
+//              (global_load_lds, swizzled rows) in super-chunks of KS*64
+//              columns through a ring of slots shared by the 4 waves;
+//              16x16x32 bf16 MFMA, fp32 accumulate; with KS > 1 the waves
+//              split the d axis and their partial tiles are summed in LDS
+//              in a fixed order;
 //        f32:  one (token, expert) dot product per thread;
 //        logits_in: copied.
-//   2. per token, a segment of S = pow2ceil(E) lanes (<= 64) holds the E logits;
-//      k+1 rounds of segment arg-max by xor-shuffles give the picks in order
-//      (ties: lower expert index). If two adjacent values among the top (k+1)
-//      are closer than BMOE_ROUTE_RECHECK_GAP the token is queued for step 3.
-//      Otherwise softmax, optional renormalisation, the map and the per-group
-//      merge are done by the k slot lanes and written out.
-//   3. a queued token is decided again in float64: every expert whose fp32 logit
-//      is within the gap of the k-th value is recomputed from exact float64
-//      products (a whole wave per expert), and the top-k is picked among those.
+//   2. per token, a group of S lanes (S <= 16, chosen so that a wave's tokens
+//      fill it) holds the E logits; k+1 rounds of group arg-max (DPP within
+//      rows of 16 lanes) give the picks in order (ties: lower expert index).
+//      If two adjacent values among the top k+1 are closer than
+//      BMOE_ROUTE_RECHECK_GAP the token is queued for step 3. Otherwise
+//      softmax, optional renormalisation, the map and the per-group merge
+//      are done from the token's pick list and written out.
+//   3. a queued token is decided again in float64 by the wave that queued it:
+//      every expert whose fp32 logit is within the gap of the k-th value is
+//      recomputed from exact float64 products, and the top-k is taken among
+//      those by ranking them.
 #include "bmoe_common.h"
 
 namespace bmoe {
@@ -31,20 +34,46 @@ constexpr int kMaxK = BMOE_MAX_TOPK;
 enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2 };
 
 struct RouteSmem {
-    int bt, zstride, e_pad, ks;
-    size_t zs_bytes, flag_bytes, wbuf_bytes;
-    __host__ __device__ size_t total() const { return zs_bytes + flag_bytes + wbuf_bytes; }
+    int zstride;
+    size_t zs_bytes, flag_bytes, cand_bytes, dummy_bytes, ring_bytes;
+    __host__ __device__ size_t total() const { return zs_bytes + flag_bytes + cand_bytes + dummy_bytes + ring_bytes; }
 };
 
-__host__ __device__ inline RouteSmem route_smem(int mode, int tb, int nblk, int E) {
+template <int TB, int NBLK>
+struct RouteCfg {
+    static constexpr int BT = 16 * TB, KS = 4 / TB, KC = 64 * KS, EP = 16 * NBLK;
+    static constexpr int CPR = KC / 8;                // 16-byte chunks per LDS row
+    static constexpr int RPD = 64 / CPR;              // rows per DMA instruction (1 KB)
+    static constexpr int SWZ = CPR >= 16 ? 15 : 7;    // swizzle mask of the chunk index
+    static constexpr int ROWB = KC * 2;
+    static constexpr int XDMA = BT / RPD, WDMA = EP / RPD, TOT = XDMA + WDMA;
+    static constexpr int DPW = (TOT + 3) / 4;         // DMA instructions per wave per slot
+    static constexpr int SLOT = (BT + EP) * ROWB;
+    static constexpr int ZS = (BT * (EP + 1) * 4 + 15) / 16 * 16;
+    static constexpr int FLAG = 2048;              // queue of near-tie tokens + map
+    static constexpr int DUMMY = 4 * 1024;            // 1 KB per wave for padding copies
+    static constexpr int CAND = 4 * 2048;             // per-wave picks / candidate lists
+    static constexpr int NSLOT_FIT = (160 * 1024 - ZS - FLAG - CAND - DUMMY) / SLOT;
+    static constexpr int NSLOT = NSLOT_FIT > 8 ? 8 : NSLOT_FIT;
+    static constexpr int PART = (KS - 1) * BT * EP * 4;
+    static constexpr int TOTAL = ZS + FLAG + CAND + DUMMY + NSLOT * SLOT;
+    static_assert(NSLOT >= 2, "at least two slots");
+    static_assert(PART <= NSLOT * SLOT, "partials alias the ring");
+    static_assert(TOTAL <= 160 * 1024, "LDS of one workgroup");
+    static_assert(DPW * (NSLOT - 2) <= 63, "vmcnt range");
+};
+
+template <int MODE, int TB, int NBLK>
+__host__ __device__ inline RouteSmem route_smem(int E) {
     RouteSmem s;
-    s.bt = 16 * tb;
-    s.e_pad = (mode == MODE_BF16) ? 16 * nblk : ((E + 15) / 16) * 16;
-    s.zstride = s.e_pad + 1;
-    s.ks = 4 / tb;
-    s.zs_bytes = ((size_t)s.bt * s.zstride * 4 + 15) / 16 * 16;
-    s.flag_bytes = 1024;
-    s.wbuf_bytes = (mode == MODE_BF16) ? (size_t)2 * s.e_pad * (s.ks * 64 + 8) * 2 : 0;
+    const int bt = 16 * TB;
+    const int e_pad = (MODE == MODE_BF16) ? 16 * NBLK : ((E + 15) / 16) * 16;
+    s.zstride = e_pad + 1;
+    s.zs_bytes = ((size_t)bt * s.zstride * 4 + 15) / 16 * 16;
+    s.flag_bytes = 2048;
+    s.cand_bytes = 4 * 2048;
+    s.dummy_bytes = (MODE == MODE_BF16) ? 4 * 1024 : 0;
+    s.ring_bytes = (MODE == MODE_BF16) ? (size_t)RouteCfg<TB, NBLK>::NSLOT * RouteCfg<TB, NBLK>::SLOT : 0;
     return s;
 }
 
@@ -55,178 +84,365 @@ __device__ __forceinline__ bool better(double v, int e, double bv, int be) {
     return v > bv || (v == bv && e < be);
 }
 
-template <typename V>
-__device__ __forceinline__ void seg_argmax(V& bv, int& be, int S) {
-    for (int off = 1; off < S; off <<= 1) {
+// ---- lane exchanges. Within rows of 16 lanes, DPP row permutations (quad
+// xor 1, quad xor 2, half-row mirror, row mirror) run on the VALU; they pair
+// every lane with a lane of the other half of its group at each step, so
+// after log2(S) steps all S lanes of an aligned group hold the reduction.
+// Steps across rows (16, 32) go through ds_bpermute (__shfl_xor).
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+    return __hiloint2double(dpp_i<CTRL>(__double2hiint(v)), dpp_i<CTRL>(__double2loint(v)));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int CTRL, typename V>
+__device__ __forceinline__ void argmax_step(V& bv, int& be) {
+    V ov;
+    if constexpr (sizeof(V) == 8) ov = dpp_d<CTRL>(bv);
+    else ov = dpp_f<CTRL>(bv);
+    const int oe = dpp_i<CTRL>(be);
+    if (better(ov, oe, bv, be)) { bv = ov; be = oe; }
+}
+
+// arg-max (ties: lower index) over aligned groups of S lanes, S in {1,2,4,...,64}
+template <int S, typename V>
+__device__ __forceinline__ void group_argmax(V& bv, int& be) {
+    if constexpr (S >= 2) argmax_step<kDppXor1>(bv, be);
+    if constexpr (S >= 4) argmax_step<kDppXor2>(bv, be);
+    if constexpr (S >= 8) argmax_step<kDppHalfMirror>(bv, be);
+    if constexpr (S >= 16) argmax_step<kDppMirror>(bv, be);
+#pragma unroll
+    for (int off = 16; off < S; off <<= 1) {
         V ov = __shfl_xor(bv, off);
         int oe = __shfl_xor(be, off);
         if (better(ov, oe, bv, be)) { bv = ov; be = oe; }
     }
 }
 
-template <typename V>
-__device__ __forceinline__ V seg_sum(V v, int S) {
-    for (int off = 1; off < S; off <<= 1) v += __shfl_xor(v, off);
+// sum over aligned groups of S lanes (every lane gets the same bits: each
+// step adds two values in an order-independent way)
+template <int S, typename V>
+__device__ __forceinline__ V group_sum(V v) {
+    if constexpr (sizeof(V) == 8) {
+        if constexpr (S >= 2) v += dpp_d<kDppXor1>(v);
+        if constexpr (S >= 4) v += dpp_d<kDppXor2>(v);
+        if constexpr (S >= 8) v += dpp_d<kDppHalfMirror>(v);
+        if constexpr (S >= 16) v += dpp_d<kDppMirror>(v);
+    } else {
+        if constexpr (S >= 2) v += dpp_f<kDppXor1>(v);
+        if constexpr (S >= 4) v += dpp_f<kDppXor2>(v);
+        if constexpr (S >= 8) v += dpp_f<kDppHalfMirror>(v);
+        if constexpr (S >= 16) v += dpp_f<kDppMirror>(v);
+    }
+#pragma unroll
+    for (int off = 16; off < S; off <<= 1) v += __shfl_xor(v, off);
     return v;
 }
 
-// Softmax weight, renormalisation, map and merge for the k slot lanes of a
-// segment; lane s (< k) holds pick s. Writes the token's outputs.
-template <typename V>
-__device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, int S, int pick,
-                                             V pick_val, V top, V sum_exp, bool write) {
-    const int k = p.k;
-    float w = 0.f;
-    if (s < k) {
-        if constexpr (sizeof(V) == 8) w = (float)(exp(pick_val - top) / sum_exp);
-        else w = expf(pick_val - top) / sum_exp;
-    }
-    if (p.norm) {
-        float tot = seg_sum(s < k ? w : 0.f, S);
-        w = w / tot;
-    }
-    int g = (s < k) ? p.e2g[pick] : -2;
-    if (s < k && (g < 0 || g >= p.G)) g = -1;  // unvalidated map entry: no call
-    bool dup = false;
-    float gate = 0.f;
-    for (int j = 0; j < k; ++j) {
-        int gj = __shfl(g, j, S);
-        float wj = __shfl(w, j, S);
-        if (j < s && gj == g) dup = true;
-        if (j >= s && gj == g) gate += wj;
-    }
-    if (write && s < k) {
-        size_t o = (size_t)t * k + s;
-        p.topk_idx[o] = pick;
-        p.topk_w[o] = w;
-        bool valid = !dup && g >= 0;
-        p.slot_group[o] = valid ? g : -1;
-        p.slot_gate[o] = valid ? gate : 0.f;
-    }
+// A pick in a token's pick list: expert id in the low 16 bits, united expert + 1
+// in the high bits (0: the map sends the expert nowhere, so the slot calls none).
+__device__ __forceinline__ int pack_pick(int e, const int* e2g_s, int E) {
+    const int g = (unsigned)e < (unsigned)E ? e2g_s[e] : -1;  // NaN logits pick nothing
+    return (e & 0xffff) | ((g + 1) << 16);
 }
 
-// Exact-product float64 dot product of one token row and one router row;
-// every lane of the wave takes 8-element chunks; the result is in all lanes.
-template <int MODE>
-__device__ __forceinline__ double dot_f64(const void* xr, const void* wr, int d, int lane) {
-    double acc = 0.0;
-    const int nch = d / 8;
-    for (int c = lane; c < nch; c += kWave) {
-        if constexpr (MODE == MODE_BF16) {
-            uint4 xv = *((const uint4*)xr + c);
-            uint4 wv = *((const uint4*)wr + c);
-            const uint16_t* xs = (const uint16_t*)&xv;
-            const uint16_t* ws = (const uint16_t*)&wv;
+// Softmax weights, optional renormalisation and per-group merge of one token
+// from its pick list (pk: packed picks, pkv: their logits, largest first),
+// shared by the S lanes of the token's group; lane s writes slots s, s+S, ...
+// (at most 4 of them: S >= 4 or S >= k). The weight of a pick is
+// exp(v - top) / sum_exp, or exp(v - top) / sum over the k picks when the top-k
+// weights are renormalised. Exponents are taken in fp32 of the difference,
+// far below the gate tolerance.
+template <typename V>
+__device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, int S, const int* pk, const V* pkv,
+                                             V top, float sum_exp, bool write) {
+    const int k = p.k;
+    int gq[4];
+    float eq[4], gs[4];
+    bool dup[4];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc += (double)bf16_to_f32(xs[i]) * (double)bf16_to_f32(ws[i]);
-        } else {
-            const float4* xf = (const float4*)xr + 2 * c;
-            const float4* wf = (const float4*)wr + 2 * c;
+    for (int i = 0; i < 4; ++i) {
+        const int q = s + i * S;
+        gq[i] = q < k ? (pk[q] >> 16) - 1 : -3;
+        eq[i] = 0.f;
+        gs[i] = 0.f;
+        dup[i] = false;
+    }
+    float tot = 0.f;
+#pragma unroll 4
+    for (int j = 0; j < k; ++j) {
+        const int g = (pk[j] >> 16) - 1;
+        const float ex = __expf((float)(pkv[j] - top));
+        tot += ex;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                float4 a = xf[h], b = wf[h];
-                acc += (double)a.x * (double)b.x;
-                acc += (double)a.y * (double)b.y;
-                acc += (double)a.z * (double)b.z;
-                acc += (double)a.w * (double)b.w;
+        for (int i = 0; i < 4; ++i) {
+            const int q = s + i * S;
+            if (j == q) eq[i] = ex;
+            if (g == gq[i]) {
+                if (j < q) dup[i] = true;
+                else gs[i] += ex;
             }
         }
     }
-    return seg_sum(acc, kWave);
-}
-
-template <int WPT, int KC, int WCH>
-__device__ __forceinline__ void route_load_w(uint4 (&wreg)[WPT], const uint16_t* w, int E, int d,
-                                             int c, int tid) {
+    if (!write) return;
+    const float inv = 1.f / (p.norm ? tot : sum_exp);
 #pragma unroll
-    for (int i = 0; i < WPT; ++i) {
-        int idx = tid + kRouteThreads * i;
-        int er = idx / (KC / 8), cc = idx % (KC / 8);
-        int col = c * KC + cc * 8;
-        wreg[i] = (idx < WCH && er < E && col < d) ? *(const uint4*)(w + (size_t)er * d + col)
-                                                   : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+        const int q = s + i * S;
+        if (q >= k) break;
+        const size_t o = (size_t)t * k + q;
+        p.topk_idx[o] = pk[q] & 0xffff;
+        p.topk_w[o] = eq[i] * inv;
+        const bool valid = !dup[i] && gq[i] >= 0;
+        p.slot_group[o] = valid ? gq[i] : -1;
+        p.slot_gate[o] = valid ? gs[i] * inv : 0.f;
     }
 }
 
-template <int WPT, int KC, int WCH, int EP, int WROW>
-__device__ __forceinline__ void route_store_w(const uint4 (&wreg)[WPT], uint16_t* wb, int buf, int tid) {
+// Step 2 for the TPW tokens of one wave. Groups of S lanes are independent
+// (their exchanges stay inside the group), so a group without a token idles.
+struct SelectCtx {
+    const float* zs;
+    int zstride;
+    int* area;        // the wave's pick area: 32 words per token
+    const int* e2g_s;
+    int* fl_count;    // the wave's queue of near-tie tokens
+    int* fl_tok;
+    float* fl_thr;
+    int t0, tw0;      // first token of the workgroup, first local row of the wave
+    bool recheck;
+};
+
+template <int S, int TPW>
+__device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCtx& c, int lane) {
+    constexpr int P = kWave / S;
+    const int E = p.E, k = p.k;
+    const int VPL = (E + S - 1) / S;
+    const int s = lane % S, seg = lane / S;
+    const int R = min(k + 1, E);
+    constexpr int kNone = 0x7fffffff;
+    for (int base = 0; base < TPW; base += P) {
+        const int tw = base + seg;
+        if (tw >= TPW) continue;
+        const bool tok_ok = c.t0 + c.tw0 + tw < p.T;
+        const int tl = tok_ok ? c.tw0 + tw : 0;
+        float v[16];
 #pragma unroll
-    for (int i = 0; i < WPT; ++i) {
-        int idx = tid + kRouteThreads * i;
-        if (idx < WCH) {
-            int er = idx / (KC / 8), cc = idx % (KC / 8);
-            *(uint4*)(wb + ((size_t)buf * EP + er) * WROW + cc * 8) = wreg[i];
+        for (int j = 0; j < 16; ++j) {
+            const int e = s + j * S;
+            v[j] = -INFINITY;
+            if (j < VPL) v[j] = e < E ? c.zs[tl * c.zstride + e] : -INFINITY;
+        }
+        // the picks go to the pick area (every lane of the group writes the
+        // same values); registers indexed by the round would need dynamic
+        // register indexing
+        int* pk = c.area + tw * 32;
+        float* pkv = (float*)(pk + 16);
+        unsigned taken = 0;
+        float prev = 0.f, top = 0.f, kth = 0.f;
+        bool close = false;
+        for (int r = 0; r < R; ++r) {
+            // local arg-max in ascending expert order: strict > keeps the lower
+            // index on ties; padding lanes hold -inf and lose to any expert
+            float bv = -INFINITY;
+            int be = kNone;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                if (j < VPL) {
+                    const bool t = !((taken >> j) & 1u) && (v[j] > bv || be == kNone);
+                    bv = t ? v[j] : bv;
+                    be = t ? s + j * S : be;
+                }
+            }
+            group_argmax<S>(bv, be);
+            if (be % S == s) taken |= 1u << (be / S);
+            if (r < k) {
+                pk[r] = pack_pick(be, c.e2g_s, E);
+                pkv[r] = bv;
+            }
+            if (r == 0) top = bv;
+            if (r == k - 1) kth = bv;
+            if (r > 0 && prev - bv < kGap) close = true;
+            prev = bv;
+        }
+        close = close && c.recheck;
+        float se = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (j < VPL) se += __expf(v[j] - top);
+        se = group_sum<S>(se);
+        finish_token<float>(p, c.t0 + tl, s, S, pk, pkv, top, se, tok_ok && !close);
+        if (tok_ok && close && s == 0) {
+            const int pos = atomicAdd(c.fl_count, 1);
+            c.fl_tok[pos] = tl;
+            c.fl_thr[pos] = kth - kGap;
         }
     }
 }
 
-template <int KC>
-__device__ __forceinline__ void route_load_a(const uint16_t* xr, int d, int c, int ks, int q,
-                                             uint4& a0, uint4& a1) {
-    int col = c * KC + ks * 64 + 16 * q;
-    a0 = col < d ? *(const uint4*)(xr + col) : make_uint4(0, 0, 0, 0);
-    a1 = col + 8 < d ? *(const uint4*)(xr + col + 8) : make_uint4(0, 0, 0, 0);
+// Exact-product float64 dot products of one token row with up to 8 router rows
+// (ids[i] < 0: unused; the used ids come first). bf16 and fp32 products are
+// exact in float64. Lane l takes the 16-byte chunks l, l+64, ... of the rows
+// (coalesced); a block of 4 chunks per lane is loaded together with the same
+// chunks of four router rows, so a token with up to 4 candidates costs one
+// memory latency per 2048 bf16 columns; each lane sums its chunks in order,
+// then the wave reduces.
+template <int MODE>
+__device__ __forceinline__ void dot_f64_batch(const char* xr, const char* w, size_t row_bytes,
+                                              const int (&ids)[8], int lane, double (&out)[8]) {
+    constexpr int U = 4;
+    constexpr int EPC = MODE == MODE_BF16 ? 8 : 4;  // elements per 16-byte chunk
+    double acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.0;
+    const int nch = (int)(row_bytes / 16);
+    for (int c0 = 0; c0 < nch; c0 += kWave * U) {
+        uint4 xv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * kWave + lane;
+            xv[u] = c < nch ? *(const uint4*)(xr + (size_t)c * 16) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll 1
+        for (int ib = 0; ib < 8; ib += 4) {
+            if (ids[ib] < 0) break;
+            uint4 wv[4][U];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int c = c0 + u * kWave + lane;
+                    wv[i][u] = (ids[ib + i] >= 0 && c < nch)
+                                   ? *(const uint4*)(w + (size_t)ids[ib + i] * row_bytes + (size_t)c * 16)
+                                   : make_uint4(0, 0, 0, 0);
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if constexpr (MODE == MODE_BF16) {
+                        const uint16_t* xs = (const uint16_t*)&xv[u];
+                        const uint16_t* ws = (const uint16_t*)&wv[i][u];
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e)
+                            acc[ib + i] += (double)bf16_to_f32(xs[e]) * (double)bf16_to_f32(ws[e]);
+                    } else {
+                        const float* xs = (const float*)&xv[u];
+                        const float* ws = (const float*)&wv[i][u];
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) acc[ib + i] += (double)xs[e] * (double)ws[e];
+                    }
+                }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) out[i] = ids[i] >= 0 ? group_sum<kWave>(acc[i]) : 0.0;
+}
+
+// copies of super-chunk c into ring slot `slot` (padding copies go to the wave's dummy area)
+template <class C>
+__device__ __forceinline__ void route_issue(const uint16_t* const (&src)[C::DPW], const int (&lcol)[C::DPW],
+                                            const uint32_t (&ldst)[C::DPW], const bool (&real)[C::DPW],
+                                            uint32_t ring0, uint32_t dummy0, int d, int c, int slot) {
+#pragma unroll
+    for (int j = 0; j < C::DPW; ++j) {
+        int col = c * C::KC + lcol[j];
+        if (col >= d) col = 0;
+        const uint32_t dst = real[j] ? ring0 + slot * C::SLOT + ldst[j] : dummy0;
+        dma16(src[j] + col, __builtin_amdgcn_readfirstlane(dst));
+    }
 }
 
 template <int TB, int NBLK>
-__device__ __forceinline__ void logits_bf16(const RouteArgs& p, const RouteSmem& sm, float* zs,
-                                            char* wraw, int t0) {
-    constexpr int KS = 4 / TB;
-    constexpr int KC = KS * 64;
-    constexpr int WROW = KC + 8;
-    constexpr int EP = NBLK * 16;
-    constexpr int WCH = EP * KC / 8;                 // 16-byte chunks per super-chunk
-    constexpr int WPT = (WCH + kRouteThreads - 1) / kRouteThreads;
+__device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char* ring, char* dummy, int t0) {
+    using C = RouteCfg<TB, NBLK>;
     const uint16_t* x = (const uint16_t*)p.x;
     const uint16_t* w = (const uint16_t*)p.w;
-    uint16_t* wb = (uint16_t*)wraw;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int tb = wave % TB, ks = wave / TB;
     const int q = lane >> 4, r16 = lane & 15;
-    const int d = p.d, E = p.E;
-    int row = t0 + tb * 16 + r16;
-    if (row > p.T - 1) row = p.T - 1;
-    const uint16_t* xr = x + (size_t)row * d;
-    const int nsc = ceil_div(d, KC);
-    const uint4 zero = make_uint4(0, 0, 0, 0);
+    const int d = p.d, E = p.E, T = p.T;
+    const int nsc = ceil_div(d, C::KC);
+    const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
+    const uint32_t dummy0 = (uint32_t)(uintptr_t)dummy + wave * 1024;
 
-    uint4 wreg[WPT];
+    // per-lane copy sources of this wave's DMA instructions (column 0 of the super-chunk)
+    const uint16_t* src[C::DPW];
+    int lcol[C::DPW];      // logical column of this lane's chunk inside a super-chunk
+    uint32_t ldst[C::DPW]; // LDS offset of the instruction inside a slot (or the dummy area)
+    bool real[C::DPW];
+    const int lrow = lane / C::CPR, lchk = lane % C::CPR;
+#pragma unroll
+    for (int j = 0; j < C::DPW; ++j) {
+        const int g = wave + 4 * j;
+        real[j] = g < C::TOT;
+        if (g < C::XDMA) {
+            const int rl = g * C::RPD + lrow;
+            const int row = min(t0 + rl, T - 1);
+            lcol[j] = (lchk ^ (rl & C::SWZ)) * 8;
+            src[j] = x + (size_t)row * d;
+            ldst[j] = g * C::RPD * C::ROWB;
+        } else if (g < C::TOT) {
+            const int rl = (g - C::XDMA) * C::RPD + lrow;
+            const int row = min(rl, E - 1);
+            lcol[j] = (lchk ^ (rl & C::SWZ)) * 8;
+            src[j] = w + (size_t)row * d;
+            ldst[j] = (C::BT + (g - C::XDMA) * C::RPD) * C::ROWB;
+        } else {
+            lcol[j] = 0;
+            src[j] = x + (size_t)min(t0, T - 1) * d;
+            ldst[j] = 0;
+        }
+    }
     f32x4 acc[NBLK];
 #pragma unroll
     for (int nb = 0; nb < NBLK; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int arow = tb * 16 + r16;
+    const int c0 = ks * 8 + 2 * q;  // logical chunks c0, c0+1 of this lane's A and B fragments
+    const int pa0 = ((c0 ^ (arow & C::SWZ)) << 4), pa1 = (((c0 + 1) ^ (arow & C::SWZ)) << 4);
+    const int pb0 = ((c0 ^ (r16 & C::SWZ)) << 4), pb1 = (((c0 + 1) ^ (r16 & C::SWZ)) << 4);
 
-    uint4 a0, a1;
-    route_load_w<WPT, KC, WCH>(wreg, w, E, d, 0, tid);
-    route_load_a<KC>(xr, d, 0, ks, q, a0, a1);
-    route_store_w<WPT, KC, WCH, EP, WROW>(wreg, wb, 0, tid);
-    __syncthreads();
+    // prologue: super-chunks 0 .. NSLOT-2 in flight
+#pragma unroll
+    for (int c = 0; c < C::NSLOT - 1; ++c)
+        if (c < nsc) route_issue<C>(src, lcol, ldst, real, ring0, dummy0, d, c, c);
+    int slot = 0;
     for (int c = 0; c < nsc; ++c) {
-        uint4 n0 = zero, n1 = zero;
-        const bool more = c + 1 < nsc;
-        if (more) {
-            route_load_w<WPT, KC, WCH>(wreg, w, E, d, c + 1, tid);
-            route_load_a<KC>(xr, d, c + 1, ks, q, n0, n1);
-        }
-        const uint16_t* wbc = wb + (size_t)(c & 1) * EP * WROW;
+        // copies issued so far: super-chunks 0 .. min(nsc-1, c+NSLOT-2)
+        wait_vmcnt_rt<C::DPW>(min(nsc - 1 - c, C::NSLOT - 2));
+        lds_reads_done();
+        wg_barrier();
+        // the slot read in the previous step is free for super-chunk c+NSLOT-1
+        const int fill = c + C::NSLOT - 1;
+        if (fill < nsc) route_issue<C>(src, lcol, ldst, real, ring0, dummy0, d, fill, slot == 0 ? C::NSLOT - 1 : slot - 1);
+        const char* base = ring + slot * C::SLOT;
+        const int col0 = c * C::KC + c0 * 8;
+        uint4 a0 = *(const uint4*)(base + arow * C::ROWB + pa0);
+        uint4 a1 = *(const uint4*)(base + arow * C::ROWB + pa1);
+        if (col0 >= d) a0 = make_uint4(0, 0, 0, 0);
+        if (col0 + 8 >= d) a1 = make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int nb = 0; nb < NBLK; ++nb) {
-            const uint16_t* bp = wbc + (nb * 16 + r16) * WROW + ks * 64 + 16 * q;
-            uint4 b0 = *(const uint4*)bp;
-            uint4 b1 = *(const uint4*)(bp + 8);
-            acc[nb] = mfma16(a0, b0, acc[nb]);
-            acc[nb] = mfma16(a1, b1, acc[nb]);
+            const char* bp = base + (C::BT + nb * 16 + r16) * C::ROWB;
+            acc[nb] = mfma16(a0, *(const uint4*)(bp + pb0), acc[nb]);
+            acc[nb] = mfma16(a1, *(const uint4*)(bp + pb1), acc[nb]);
         }
-        if (more) {
-            route_store_w<WPT, KC, WCH, EP, WROW>(wreg, wb, (c + 1) & 1, tid);
-            a0 = n0;
-            a1 = n1;
-        }
-        __syncthreads();
+        slot = slot + 1 == C::NSLOT ? 0 : slot + 1;
     }
+    wait_vmcnt<0>();
+    __syncthreads();
 
-    // partial tiles of the d-split waves are summed in LDS (reusing the W buffer)
-    float* part = (float*)wraw;
-    const int BT = 16 * TB;
+    // partial tiles of the d-split waves are summed in LDS (reusing the ring)
+    float* part = (float*)ring;
+    constexpr int BT = C::BT, EP = C::EP, KS = C::KS;
     if (KS > 1 && ks > 0) {
 #pragma unroll
         for (int nb = 0; nb < NBLK; ++nb)
@@ -244,7 +460,7 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, const RouteSmem&
                 const int tl = tb * 16 + 4 * q + i;
                 for (int kk = 1; kk < KS; ++kk) v += part[((size_t)(kk - 1) * BT + tl) * EP + nb * 16 + r16];
                 const int e = nb * 16 + r16;
-                if (e < E) zs[tl * sm.zstride + e] = v + (p.bias ? p.bias[e] : 0.f);
+                if (e < E) zs[tl * (EP + 1) + e] = v + (p.bias ? p.bias[e] : 0.f);
             }
     }
 }
@@ -252,22 +468,31 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, const RouteSmem&
 template <int MODE, int TB, int NBLK>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     extern __shared__ __align__(16) char smem[];
-    const RouteSmem sm = route_smem(MODE, TB, NBLK, p.E);
+    const RouteSmem sm = route_smem<MODE, TB, NBLK>(p.E);
     constexpr int BT = 16 * TB;
     constexpr int TPW = BT / 4;  // tokens per wave in the selection steps
+    static_assert(TPW * 32 <= 512, "pick area of a wave");
     float* zs = (float*)smem;
     int* fl_count = (int*)(smem + sm.zs_bytes);
     int* fl_tok = fl_count + 4;
     float* fl_thr = (float*)(fl_tok + 4 * 16);
-    char* wraw = smem + sm.zs_bytes + sm.flag_bytes;
+    char* dummy = smem + sm.zs_bytes + sm.flag_bytes + sm.cand_bytes;
+    char* ring = dummy + sm.dummy_bytes;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    // per-wave area: picks of the wave's tokens (step 2), then candidate lists (step 3)
+    int* cl = (int*)(smem + sm.zs_bytes + sm.flag_bytes) + wave * 512;
     const int t0 = blockIdx.x * BT;
     const int T = p.T, E = p.E, k = p.k;
+    int* e2g_s = (int*)(smem + sm.zs_bytes + 1024);  // map, invalid entries -> -1
     if (tid < 4) fl_count[tid] = 0;
+    for (int i = tid; i < E; i += kRouteThreads) {
+        const int g = p.e2g[i];
+        e2g_s[i] = (g >= 0 && g < p.G) ? g : -1;
+    }
 
     // ---- 1. logits tile
     if constexpr (MODE == MODE_BF16) {
-        logits_bf16<TB, NBLK>(p, sm, zs, wraw, t0);
+        logits_bf16<TB, NBLK>(p, zs, ring, dummy, t0);
     } else if constexpr (MODE == MODE_F32) {
         const float* x = (const float*)p.x;
         const float* w = (const float*)p.w;
@@ -296,135 +521,157 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     }
 
     // ---- 2. selection on the fp32 logits
-    int S = 1;
-    while (S < E && S < 64) S <<= 1;
-    const int VPL = ceil_div(E, S);
-    const int P = kWave / S;
-    const int s = lane % S, seg = lane / S;
-    const int R = min(k + 1, E);
-    const bool recheck = (MODE != MODE_LOGITS_IN);
-    for (int base = 0; base < TPW; base += P) {
-        const int tw = base + seg;
-        const bool tok_ok = tw < TPW && t0 + wave * TPW + tw < T;
-        const int tl = tok_ok ? wave * TPW + tw : 0;
-        float v[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            int e = s + S * j;
-            v[j] = (j < VPL && e < E) ? zs[tl * sm.zstride + e] : -INFINITY;
-        }
-        unsigned taken = 0;
-        float prev = 0.f, top = 0.f, kth = 0.f, my_val = 0.f;
-        int my_pick = 0;
-        bool close = false;
-        for (int r = 0; r < R; ++r) {
-            float bv = -INFINITY;
-            int be = 0x7fffffff;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                int e = s + S * j;
-                if (j < VPL && e < E && !((taken >> j) & 1u) && better(v[j], e, bv, be)) {
-                    bv = v[j];
-                    be = e;
-                }
-            }
-            seg_argmax(bv, be, S);
-            if (be % S == s) taken |= 1u << (be / S);
-            if (s == r) { my_pick = be; my_val = bv; }
-            if (r == 0) top = bv;
-            if (r == k - 1) kth = bv;
-            if (r > 0 && prev - bv < kGap) close = true;
-            prev = bv;
-        }
-        close = close && recheck;
-        float se = 0.f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            int e = s + S * j;
-            if (j < VPL && e < E) se += expf(v[j] - top);
-        }
-        se = seg_sum(se, S);
-        finish_token<float>(p, t0 + tl, s, S, my_pick, my_val, top, se, tok_ok && !close);
-        if (tok_ok && close && s == 0) {
-            int pos = atomicAdd(&fl_count[wave], 1);
-            fl_tok[wave * 16 + pos] = tl;
-            fl_thr[wave * 16 + pos] = kth - kGap;
+    // A token occupies an aligned group of S lanes, S chosen so that the wave's
+    // TPW tokens fill the wave in one pass where E allows (at most 16 values per
+    // lane); lane s holds experts s, s+S, s+2S, ... .
+    {
+        int S = 1;
+        while (S < E && S * TPW < kWave) S <<= 1;
+        while (S * 16 < E) S <<= 1;
+        SelectCtx c{zs, sm.zstride, cl, e2g_s, fl_count + wave, fl_tok + wave * 16, fl_thr + wave * 16,
+                    t0, wave * TPW, MODE != MODE_LOGITS_IN};
+        switch (S) {
+            case 1: select_tokens<1, TPW>(p, c, lane); break;
+            case 2: select_tokens<2, TPW>(p, c, lane); break;
+            case 4: select_tokens<4, TPW>(p, c, lane); break;
+            case 8: select_tokens<8, TPW>(p, c, lane); break;
+            default: select_tokens<16, TPW>(p, c, lane); break;
         }
     }
-    __syncthreads();
 
-    // ---- 3. float64 decision for queued tokens (one wave per token)
+    // ---- 3. float64 decision for this wave's queued tokens (one wave per token)
+    // Only experts whose fp32 logit is within the gap of the k-th value can be
+    // in the exact top-k (the fp32 logits are far more accurate than the gap);
+    // they are recomputed from exact float64 products and the picks are taken
+    // among them. The queue is the wave's own, so no workgroup barrier.
     if constexpr (MODE != MODE_LOGITS_IN) {
+        lds_reads_done();
         const int nf = fl_count[wave];
         const size_t xrow_bytes = (size_t)p.d * (MODE == MODE_BF16 ? 2 : 4);
+        // wave area: candidate ids [0, 1 KB), their exact logits (up to 32) at
+        // 1 KB, the pick list at 1280 B (16 packed picks, 16 logits)
+        double* cz = (double*)(cl + 256);
+        int* pk3 = cl + 320;
+        double* pv3 = (double*)(cl + 336);
         for (int f = 0; f < nf; ++f) {
             const int tl = fl_tok[wave * 16 + f];
             const float thr = fl_thr[wave * 16 + f];
             const int t = t0 + tl;
             const char* xr = (const char*)p.x + (size_t)t * xrow_bytes;
-            double zz[4];
             float fz[4];
             bool cand[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                int e = lane + kWave * j;
+                const int e = lane + kWave * j;
                 fz[j] = e < E ? zs[tl * sm.zstride + e] : -INFINITY;
                 cand[j] = e < E && fz[j] >= thr;
-                zz[j] = -INFINITY;
             }
-            unsigned long long mk[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) mk[j] = __ballot(cand[j]);
-            for (int j = 0; j < 4; ++j) {
-                unsigned long long m = j == 0 ? mk[0] : j == 1 ? mk[1] : j == 2 ? mk[2] : mk[3];
-                while (m) {
-                    const int b = __ffsll((long long)m) - 1;
-                    m &= m - 1;
-                    const int e = b + kWave * j;
-                    double z = dot_f64<MODE>(xr, (const char*)p.w + (size_t)e * xrow_bytes, p.d, lane);
-                    if (p.bias) z += (double)p.bias[e];
-                    if (lane == b) {
-                        if (j == 0) zz[0] = z;
-                        else if (j == 1) zz[1] = z;
-                        else if (j == 2) zz[2] = z;
-                        else zz[3] = z;
-                    }
-                }
-            }
-            unsigned taken = 0;
-            double top = 0.0, my_val = 0.0;
-            int my_pick = 0;
-            for (int r = 0; r < k; ++r) {
-                double bv = -INFINITY;
-                int be = 0x7fffffff;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    int e = lane + kWave * j;
-                    if (cand[j] && !((taken >> j) & 1u) && better(zz[j], e, bv, be)) {
-                        bv = zz[j];
-                        be = e;
-                    }
-                }
-                seg_argmax(bv, be, kWave);
-                if ((be & 63) == lane) taken |= 1u << (be >> 6);
-                if (lane == r) { my_pick = be; my_val = bv; }
-                if (r == 0) top = bv;
-            }
-            double se = 0.0;
+            // candidate list (ascending expert id) in this wave's LDS area
+            int nc = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                int e = lane + kWave * j;
-                if (e < E) se += exp((cand[j] ? zz[j] : (double)fz[j]) - top);
+                const unsigned long long m = __ballot(cand[j]);
+                if (cand[j]) cl[nc + __popcll(m & ((1ull << lane) - 1ull))] = lane + kWave * j;
+                nc += __popcll(m);
             }
-            se = seg_sum(se, kWave);
-            finish_token<double>(p, t, lane, kWave, my_pick, my_val, top, se, true);
+            lds_reads_done();
+            double top;
+            float sc = 0.f;  // this lane's softmax terms of candidates
+            if (nc <= 32) {
+                // exact logits of the candidates into LDS, eight at a time
+                for (int b0 = 0; b0 < nc; b0 += 8) {
+                    int ids[8];
+                    double z[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) ids[i] = b0 + i < nc ? cl[b0 + i] : -1;
+                    dot_f64_batch<MODE>(xr, (const char*)p.w, xrow_bytes, ids, lane, z);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+                        if (lane == i && ids[i] >= 0) cz[b0 + i] = z[i] + (p.bias ? (double)p.bias[ids[i]] : 0.0);
+                }
+                lds_reads_done();
+                // lane i ranks candidate i among all candidates (ties: lower id);
+                // the ranks are a permutation, the first k are the picks
+                double mz = -INFINITY;
+                if (lane < nc) {
+                    mz = cz[lane];
+                    const int mid = cl[lane];
+                    int rank = 0;
+                    for (int j = 0; j < nc; ++j) rank += better(cz[j], cl[j], mz, mid) ? 1 : 0;
+                    if (rank < k) {
+                        pk3[rank] = pack_pick(mid, e2g_s, E);
+                        pv3[rank] = mz;
+                    }
+                }
+                lds_reads_done();
+                top = pv3[0];
+                if (lane < nc) sc = __expf((float)(mz - top));
+            } else {
+                // many near-equal logits: candidates stay in their experts' lanes
+                double zz[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) zz[j] = -INFINITY;
+                for (int b0 = 0; b0 < nc; b0 += 8) {
+                    int ids[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) ids[i] = b0 + i < nc ? cl[b0 + i] : -1;
+                    double z[8];
+                    dot_f64_batch<MODE>(xr, (const char*)p.w, xrow_bytes, ids, lane, z);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        if (ids[i] < 0) continue;
+                        const double zi = z[i] + (p.bias ? (double)p.bias[ids[i]] : 0.0);
+                        if (lane == (ids[i] & 63)) {
+                            const int j = ids[i] >> 6;
+                            if (j == 0) zz[0] = zi;
+                            else if (j == 1) zz[1] = zi;
+                            else if (j == 2) zz[2] = zi;
+                            else zz[3] = zi;
+                        }
+                    }
+                }
+                unsigned taken = 0;
+                for (int r = 0; r < k; ++r) {
+                    double bv = -INFINITY;
+                    int be = 0x7fffffff;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int e = lane + kWave * j;
+                        if (cand[j] && !((taken >> j) & 1u) && better(zz[j], e, bv, be)) {
+                            bv = zz[j];
+                            be = e;
+                        }
+                    }
+                    group_argmax<kWave>(bv, be);
+                    if ((be & 63) == lane) taken |= 1u << (be >> 6);
+                    if (lane == 0) {
+                        pk3[r] = pack_pick(be, e2g_s, E);
+                        pv3[r] = bv;
+                    }
+                }
+                lds_reads_done();
+                top = pv3[0];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (cand[j]) sc += __expf((float)(zz[j] - top));
+            }
+            // the other experts' softmax terms from their fp32 logits
+            float so = sc;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int e = lane + kWave * j;
+                if (e < E && !cand[j]) so += __expf((float)((double)fz[j] - top));
+            }
+            so = group_sum<kWave>(so);
+            finish_token<double>(p, t, lane, kWave, pk3, pv3, top, so, true);
+            lds_reads_done();  // cl is rewritten for the next queued token
         }
     }
 }
 
 template <int MODE, int TB, int NBLK>
 hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
-    const RouteSmem sm = route_smem(MODE, TB, NBLK, a.E);
+    const RouteSmem sm = route_smem<MODE, TB, NBLK>(a.E);
     auto kern = route_kernel<MODE, TB, NBLK>;
     hipError_t err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                                          (int)sm.total());
