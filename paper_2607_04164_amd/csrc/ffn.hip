@@ -304,6 +304,11 @@ constexpr int kDmaStages = BMOE_FORCE_DMA_STAGES;
 #else
 constexpr int kDmaStages = 2;
 #endif
+#ifdef BMOE_FORCE_GROUP_M
+constexpr int kGroupM = BMOE_FORCE_GROUP_M;
+#else
+constexpr int kGroupM = 4;
+#endif
 
 
 template <bool GATED, int NSTAGE, int BKV>
@@ -340,19 +345,35 @@ __device__ __forceinline__ int swz(int row) { return (row >> 1) & (KC - 1); }
 template <class C>
 __device__ __forceinline__ int lds_off(int r, int c) { return r * C::ROW_BYTES + ((c ^ swz<C::KC>(r)) << 4); }
 
+// Copy sources of one wave: a workgroup-uniform base per operand (SGPRs) and
+// a 32-bit byte offset per lane and instruction (one VGPR each).
 template <class C>
-__device__ __forceinline__ void dma_stage(const uint16_t* const (&a_src)[C::A_DMA],
-                                          const uint16_t* const (&b_src)[C::B_DMA], uint32_t stage_lds,
-                                          int wave, int k0) {
-    // instruction i of wave w fills ROWS_PER_DMA consecutive rows (1 KB of LDS)
+struct DmaSrc {
+    const char* a_base;
+    const char* b_base;
+    uint32_t a_off[C::A_DMA];
+    uint32_t b_off[C::B_DMA];
+};
+
+// DMA instruction i of the wave's share of a stage: instructions 0..A_DMA-1
+// fill A rows, the rest B rows; instruction i of wave w fills ROWS_PER_DMA
+// consecutive rows (1 KB of LDS). kb: byte offset of the K-step in a row.
+template <class C>
+__device__ __forceinline__ void dma_one(const DmaSrc<C>& src, uint32_t stage_lds, int wave, int kb, int i) {
+    if (i < C::A_DMA) {
+        dma16s(src.a_base + kb, src.a_off[i],
+               stage_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
+    } else {
+        const int j = i - C::A_DMA;
+        dma16s(src.b_base + kb, src.b_off[j],
+               stage_lds + C::A_STAGE + ((wave * C::B_DMA + j) * C::ROWS_PER_DMA) * C::ROW_BYTES);
+    }
+}
+
+template <class C>
+__device__ __forceinline__ void dma_stage(const DmaSrc<C>& src, uint32_t stage_lds, int wave, int kb) {
 #pragma unroll
-    for (int i = 0; i < C::A_DMA; ++i)
-        dma16(a_src[i] + k0, __builtin_amdgcn_readfirstlane(
-                                 stage_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES));
-#pragma unroll
-    for (int i = 0; i < C::B_DMA; ++i)
-        dma16(b_src[i] + k0, __builtin_amdgcn_readfirstlane(
-                                 stage_lds + C::A_STAGE + ((wave * C::B_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES));
+    for (int i = 0; i < C::DMA_PER_STAGE; ++i) dma_one<C>(src, stage_lds, wave, kb, i);
 }
 
 template <class C>
@@ -380,6 +401,29 @@ __device__ __forceinline__ void dma_mfmas(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
             for (int nb = 0; nb < C::NB; ++nb) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
 }
 
+// The MFMAs of one sub-step with the wave's DMA instructions of a stage
+// spread between them, so that a DMA issue that waits for queue space does
+// not hold back a run of MFMAs.
+template <class C>
+__device__ __forceinline__ void dma_mfmas_ilv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                              const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
+                                              uint32_t stage_lds, int wave, int kb, bool do_dma) {
+    constexpr int NM = C::NMAT * C::MB * C::NB;
+    static_assert(C::DMA_PER_STAGE <= NM, "one DMA per MFMA at most");
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+        const int mat = q / (C::MB * C::NB), mb = (q / C::NB) % C::MB, nb = q % C::NB;
+        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        if (q * C::DMA_PER_STAGE % NM < C::DMA_PER_STAGE) {
+            // only the asm copy sits behind the (uniform) branch: MFMAs under
+            // control flow make the compiler shuffle the accumulators
+            __builtin_amdgcn_sched_barrier(0);
+            if (do_dma) dma_one<C>(src, stage_lds, wave, kb, q * C::DMA_PER_STAGE / NM);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
 template <bool GATED, int NSTAGE, int BKV>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmParams p) {
     using C = DmaCfg<GATED, NSTAGE, BKV>;
@@ -392,7 +436,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
     int* s_beg = s_mt + BMOE_MAX_EXPERTS + 1;
     int* s_end = s_beg + BMOE_MAX_EXPERTS;
 
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int n_seg = p.n_seg, N = p.N, K = p.K;
 
     // ---- tile schedule from the device offsets (same mapping as the other GEMMs)
@@ -418,32 +462,42 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         if (s_mt[mid] * NT <= L) lo = mid;
         else hi = mid - 1;
     }
-    const int s = lo;
-    const int mts = s_mt[s + 1] - s_mt[s];
-    const int local = L - s_mt[s] * NT;
-    const int nt = local / mts, mt = local % mts;
-    const int m0 = s_beg[s] + mt * BM, m_end = s_end[s];
+    // the schedule values come from LDS; they are workgroup-uniform, and
+    // readfirstlane lets the compiler keep them (and the copy bases) in SGPRs
+    const int s = __builtin_amdgcn_readfirstlane(lo);
+    const int mts = __builtin_amdgcn_readfirstlane(s_mt[s + 1] - s_mt[s]);
+    const int local = L - __builtin_amdgcn_readfirstlane(s_mt[s]) * NT;
+    // tiles of a segment in groups of kGroupM M-tiles, N-tiles outer within a
+    // group: the workgroups that run together on one XCD share A and B panels
+    const int mg = local / (kGroupM * NT), gm = min(kGroupM, mts - mg * kGroupM);
+    const int rem = local - mg * kGroupM * NT;
+    const int nt = rem / gm, mt = mg * kGroupM + rem % gm;
+    const int m0 = __builtin_amdgcn_readfirstlane(s_beg[s]) + mt * BM;
+    const int m_end = __builtin_amdgcn_readfirstlane(s_end[s]);
     const int n0 = nt * BN;
     __syncthreads();  // schedule arrays are overwritten by the first DMAs
 
     // ---- per-lane DMA sources: lane l of instruction i of wave w fills LDS row
     // r = (w*N_DMA + i)*ROWS_PER_DMA + l/KC, physical chunk l%KC, i.e. logical
     // chunk (l%KC) ^ swz(r); the KC lanes of a row read its contiguous bytes
-    const uint16_t* a_src[C::A_DMA];
-    const uint16_t* b_src[C::B_DMA];
+    DmaSrc<C> src;
     const int lrow = lane / C::KC, lchk = lane % C::KC;
+    src.a_base = (const char*)(p.A + (size_t)m0 * K);
 #pragma unroll
     for (int i = 0; i < C::A_DMA; ++i) {
         const int r = (wave * C::A_DMA + i) * C::ROWS_PER_DMA + lrow;
         const int row = min(m0 + r, m_end - 1);
-        a_src[i] = p.A + (size_t)row * K + ((lchk ^ swz<C::KC>(r)) << 3);
+        src.a_off[i] = (uint32_t)(((row - m0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
+    // a wave's B rows lie in one matrix (gate or up for the gated GEMM)
+    static_assert(!GATED || (C::B_DMA * C::ROWS_PER_DMA * 2 == BN), "B rows of a wave in one matrix");
+    const int bmat = GATED ? (wave * C::B_DMA * C::ROWS_PER_DMA) / BN : 0;
+    src.b_base = (const char*)((bmat ? p.B1 : p.B0) + ((size_t)s * N + n0) * K);
 #pragma unroll
     for (int i = 0; i < C::B_DMA; ++i) {
         const int r = (wave * C::B_DMA + i) * C::ROWS_PER_DMA + lrow;
-        const int mat = GATED ? r / BN : 0;
         const int n = min(n0 + r % BN, N - 1);
-        b_src[i] = (mat ? p.B1 : p.B0) + ((size_t)s * N + n) * K + ((lchk ^ swz<C::KC>(r)) << 3);
+        src.b_off[i] = (uint32_t)(((n - n0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
     const int wm = wave >> 1, wn = wave & 1;
@@ -462,7 +516,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
     // ---- prologue: the first STAGES stages in flight, wait for stage 0
 #pragma unroll
     for (int st = 0; st < C::STAGES; ++st)
-        if (st < nk) dma_stage<C>(a_src, b_src, lds0 + st * C::STAGE, wave, st * C::BK);
+        if (st < nk) dma_stage<C>(src, lds0 + st * C::STAGE, wave, st * C::BK * 2);
     wait_vmcnt_rt<C::DMA_PER_STAGE>(min(nk, C::STAGES) - 1);
     wg_barrier();
     uint4 af0[C::MB], af1[C::MB];
@@ -487,15 +541,19 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
             if (j + 1 < C::SUB) dma_frags<C>(ga, gb, stage, wm, wn, lane, j + 1);
             __builtin_amdgcn_sched_barrier(0);
-            dma_mfmas<C>(acc, fa, fb);
+            // the last sub-step carries the DMAs of stage kt+STAGES (its slot
+            // was released by the barrier of the previous sub-step)
+            if (j == C::SUB - 1)  // resolved by the unrolling
+                dma_mfmas_ilv<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK * 2,
+                                 kt + C::STAGES < nk);
+            else
+                dma_mfmas<C>(acc, fa, fb);
             __builtin_amdgcn_sched_barrier(0);
             if (j == C::SUB - 2) {
                 // stages issued so far: 0 .. min(nk-1, kt+STAGES-1); stage kt+1 must be resident
                 wait_vmcnt_rt<C::DMA_PER_STAGE>(max(0, min(nk - 1, kt + C::STAGES - 1) - (kt + 1)));
                 lds_reads_done();
                 wg_barrier();
-                if (kt + C::STAGES < nk)
-                    dma_stage<C>(a_src, b_src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK);
                 // registers of this sub-step are free now: next stage, sub-step 0
                 dma_frags<C>(fa, fb, smem + next * C::STAGE, wm, wn, lane, 0);
                 __builtin_amdgcn_sched_barrier(0);
