@@ -330,11 +330,16 @@ struct DmaCfg {
     static constexpr int SROW = WTN + 8;
     static constexpr int EPI = 4 * WTM * SROW * 2;
     static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;  // tile-schedule arrays
-    static constexpr int RING = STAGES * STAGE;
+    // NSTAGE == 5 selects the unit ring: five 32 KB slots that each hold the A
+    // half or the B half of a K-step (units A0 B0 A1 B1 ..., unit u in slot
+    // u % 5), so one and a half K-steps are in flight while one is read
+    static constexpr bool UNITS = NSTAGE == 5;
+    static constexpr int RING = UNITS ? 5 * A_STAGE : STAGES * STAGE;
     static constexpr int SMEM = (RING > EPI ? RING : EPI) > SCHED ? (RING > EPI ? RING : EPI) : SCHED;
     static_assert((KC == 4 || KC == 8) && BM == 256 && RB == 256, "tile shape");
     static_assert(SUB % 2 == 0, "fragment double buffer alternates within a stage");
     static_assert(SMEM <= 160 * 1024, "LDS of one workgroup");
+    static_assert(!UNITS || (A_STAGE == B_STAGE && A_DMA == B_DMA), "units of equal size");
 };
 
 // 16-byte chunk swizzle of a tile row: conflict-free 128-bit fragment reads
@@ -399,6 +404,85 @@ __device__ __forceinline__ void dma_mfmas(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
         for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < C::NB; ++nb) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+}
+
+// DMA instruction i of the wave's share of unit u (u even: A half of K-step
+// u/2, u odd: B half) into the slot at slot_lds.
+template <class C>
+__device__ __forceinline__ void dma_unit_one(const DmaSrc<C>& src, uint32_t slot_lds, int wave, int u, int i) {
+    const int kb = (u >> 1) * C::BK * 2;
+    if ((u & 1) == 0)
+        dma16s(src.a_base + kb, src.a_off[i], slot_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
+    else
+        dma16s(src.b_base + kb, src.b_off[i], slot_lds + ((wave * C::B_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
+}
+
+template <class C>
+__device__ __forceinline__ void dma_frags_ab(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB], const char* a_slot,
+                                             const char* b_slot, int wm, int wn, int lane, int kk) {
+    const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb)
+        af[mb] = *(const uint4*)(a_slot + lds_off<C>(wm * C::WTM + mb * 32 + l32, c));
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb)
+            bf[mat][nb] = *(const uint4*)(b_slot + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
+}
+
+// The MFMAs of one sub-step with the copies of units u0 and u1 (one copy
+// instruction after each MFMA; only the asm copy sits behind a branch).
+template <class C>
+__device__ __forceinline__ void unit_mfmas_ilv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                               const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
+                                               uint32_t lds0, int wave, int u0, int u1, int nu) {
+    constexpr int NM = C::NMAT * C::MB * C::NB;
+    static_assert(2 * C::A_DMA == NM, "one copy per MFMA");
+    const uint32_t s0 = lds0 + (u0 % 5) * C::A_STAGE, s1 = lds0 + (u1 % 5) * C::A_STAGE;
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+        const int mat = q / (C::MB * C::NB), mb = (q / C::NB) % C::MB, nb = q % C::NB;
+        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (q < C::A_DMA) {
+            if (u0 < nu) dma_unit_one<C>(src, s0, wave, u0, q);
+        } else {
+            if (u1 < nu) dma_unit_one<C>(src, s1, wave, u1, q - C::A_DMA);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// The MFMAs of one sub-step (A-fragment-major order) with the fragment reads
+// of the next sub-step spread between them, one read after every second
+// MFMA, in the order the next sub-step consumes them (all B fragments, then
+// A fragments), so that LDS returns do not arrive in one burst.
+template <class C>
+__device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                                 const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga)[C::MB],
+                                                 uint4 (&gb)[C::NMAT][C::NB], const char* a_slot,
+                                                 const char* b_slot, int wm, int wn, int lane, int kk) {
+    constexpr int NM = C::NMAT * C::MB * C::NB, NR = C::MB + C::NMAT * C::NB;
+    static_assert(2 * NR == NM, "one read per two MFMAs");
+    const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+        const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
+        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        if (q & 1) {
+            const int r = q >> 1;
+            __builtin_amdgcn_sched_barrier(0);
+            if (r < C::NMAT * C::NB) {
+                const int rm = r / C::NB, rn = r % C::NB;
+                gb[rm][rn] = *(const uint4*)(b_slot + lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
+            } else {
+                const int ra = r - C::NMAT * C::NB;
+                ga[ra] = *(const uint4*)(a_slot + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
 }
 
 // The MFMAs of one sub-step with the wave's DMA instructions of a stage
@@ -513,53 +597,99 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
 #pragma unroll
                 for (int i = 0; i < 16; ++i) acc[mat][mb][nb][i] = 0.f;
 
-    // ---- prologue: the first STAGES stages in flight, wait for stage 0
-#pragma unroll
-    for (int st = 0; st < C::STAGES; ++st)
-        if (st < nk) dma_stage<C>(src, lds0 + st * C::STAGE, wave, st * C::BK * 2);
-    wait_vmcnt_rt<C::DMA_PER_STAGE>(min(nk, C::STAGES) - 1);
-    wg_barrier();
     uint4 af0[C::MB], af1[C::MB];
     uint4 bf0[C::NMAT][C::NB], bf1[C::NMAT][C::NB];
-    dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
-
-    // The LDS reads of every K-step are unconditional (the last step reads a
-    // stale slot and drops it), so the compiler's LDS wait counts never merge
-    // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
-    // sched_barrier(0) fences keep each group of fragment reads ahead of the
-    // MFMA group that hides its latency (the scheduler would otherwise sink
-    // the next stage's reads to the top of the next iteration).
-    int slot = 0;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
-        const char* stage = smem + slot * C::STAGE;
+    if constexpr (C::UNITS) {
+        // ---- unit ring: units 0..4 in flight, wait for units 0 and 1
+        const int nu = 2 * nk;
 #pragma unroll
-        for (int j = 0; j < C::SUB; ++j) {
-            uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
-            uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
-            uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
-            uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
-            if (j + 1 < C::SUB) dma_frags<C>(ga, gb, stage, wm, wn, lane, j + 1);
-            __builtin_amdgcn_sched_barrier(0);
-            // the last sub-step carries the DMAs of stage kt+STAGES (its slot
-            // was released by the barrier of the previous sub-step)
-            if (j == C::SUB - 1)  // resolved by the unrolling
-                dma_mfmas_ilv<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK * 2,
-                                 kt + C::STAGES < nk);
-            else
-                dma_mfmas<C>(acc, fa, fb);
-            __builtin_amdgcn_sched_barrier(0);
-            if (j == C::SUB - 2) {
-                // stages issued so far: 0 .. min(nk-1, kt+STAGES-1); stage kt+1 must be resident
-                wait_vmcnt_rt<C::DMA_PER_STAGE>(max(0, min(nk - 1, kt + C::STAGES - 1) - (kt + 1)));
-                lds_reads_done();
-                wg_barrier();
-                // registers of this sub-step are free now: next stage, sub-step 0
-                dma_frags<C>(fa, fb, smem + next * C::STAGE, wm, wn, lane, 0);
+        for (int u = 0; u < 5; ++u)
+            if (u < nu)
+#pragma unroll
+                for (int i = 0; i < C::A_DMA; ++i) dma_unit_one<C>(src, lds0 + u * C::A_STAGE, wave, u, i);
+        wait_vmcnt_rt<C::A_DMA>(min(nu, 5) - 2);
+        wg_barrier();
+        dma_frags_ab<C>(af0, bf0, smem, smem + C::A_STAGE, wm, wn, lane, 0);
+        int ua = 0;  // slot of unit 2*kt (A half of the current K-step)
+        for (int kt = 0; kt < nk; ++kt) {
+            const int ub = ua == 4 ? 0 : ua + 1;
+            const int na = ub == 4 ? 0 : ub + 1, nb2 = na == 4 ? 0 : na + 1;
+            const char* a_slot = smem + ua * C::A_STAGE;
+            const char* b_slot = smem + ub * C::A_STAGE;
+#pragma unroll
+            for (int j = 0; j < C::SUB; ++j) {
+                uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
+                uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
+                uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
+                uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
+                if (j + 1 < C::SUB) dma_frags_ab<C>(ga, gb, a_slot, b_slot, wm, wn, lane, j + 1);
                 __builtin_amdgcn_sched_barrier(0);
+                // the last sub-step carries units 2kt+5 and 2kt+6, whose slots
+                // (those of the current K-step) the barrier below released
+                if (j == C::SUB - 1)  // resolved by the unrolling
+                    unit_mfmas_ilv<C>(acc, fa, fb, src, lds0, wave, 2 * kt + 5, 2 * kt + 6, nu);
+                else
+                    dma_mfmas<C>(acc, fa, fb);
+                __builtin_amdgcn_sched_barrier(0);
+                if (j == C::SUB - 2) {
+                    // units issued so far: 0 .. min(nu, 2kt+5)-1; units 2kt+2
+                    // and 2kt+3 (next K-step) must be resident
+                    wait_vmcnt_rt<C::A_DMA>(max(0, min(nu, 2 * kt + 5) - (2 * kt + 4)));
+                    lds_reads_done();
+                    wg_barrier();
+                    dma_frags_ab<C>(fa, fb, smem + na * C::A_STAGE, smem + nb2 * C::A_STAGE, wm, wn, lane, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
+            ua = na;
         }
-        slot = next;
+    } else {
+        // ---- prologue: the first STAGES stages in flight, wait for stage 0
+#pragma unroll
+        for (int st = 0; st < C::STAGES; ++st)
+            if (st < nk) dma_stage<C>(src, lds0 + st * C::STAGE, wave, st * C::BK * 2);
+        wait_vmcnt_rt<C::DMA_PER_STAGE>(min(nk, C::STAGES) - 1);
+        wg_barrier();
+        dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
+
+        // The LDS reads of every K-step are unconditional (the last step reads a
+        // stale slot and drops it), so the compiler's LDS wait counts never merge
+        // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
+        // sched_barrier(0) fences keep each group of fragment reads ahead of the
+        // MFMA group that hides its latency (the scheduler would otherwise sink
+        // the next stage's reads to the top of the next iteration).
+        int slot = 0;
+        for (int kt = 0; kt < nk; ++kt) {
+            const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
+            const char* stage = smem + slot * C::STAGE;
+#pragma unroll
+            for (int j = 0; j < C::SUB; ++j) {
+                uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
+                uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
+                uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
+                uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
+                __builtin_amdgcn_sched_barrier(0);
+                // the last sub-step carries the DMAs of stage kt+STAGES (its slot
+                // was released by the barrier of the previous sub-step); the
+                // others carry the fragment reads of the next sub-step
+                if (j == C::SUB - 1)  // resolved by the unrolling
+                    dma_mfmas_ilv<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK * 2,
+                                     kt + C::STAGES < nk);
+                else
+                    mfmas_with_reads<C>(acc, fa, fb, ga, gb, stage, stage + C::A_STAGE, wm, wn, lane, j + 1);
+                __builtin_amdgcn_sched_barrier(0);
+                if (j == C::SUB - 2) {
+                    // stages issued so far: 0 .. min(nk-1, kt+STAGES-1); stage kt+1 must be resident
+                    wait_vmcnt_rt<C::DMA_PER_STAGE>(max(0, min(nk - 1, kt + C::STAGES - 1) - (kt + 1)));
+                    lds_reads_done();
+                    wg_barrier();
+                    // registers of this sub-step are free now: next stage, sub-step 0
+                    dma_frags<C>(fa, fb, smem + next * C::STAGE, wm, wn, lane, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            slot = next;
+        }
     }
     __syncthreads();
 
