@@ -179,11 +179,23 @@ BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t*
  * y [rows_cap, d]. n_seg in 1..256. bf16: MFMA, fp32 accumulation.
  * The shared experts of a layer run through this call too, with n_seg = 1,
  * offsets = {0, T}, a = x.
+ * workspace (optional, device memory, 256-byte aligned): NULL runs one output
+ * tile per workgroup. With at least bmoe_workspace_bytes(desc,
+ * BMOE_STAGE_FFN) bytes (the size depends on the current device) the large
+ * bf16 GEMMs run one workgroup per CU and split the K loop of the last tiles
+ * so every CU gets the same work; the partial sums of a split tile meet in
+ * the workspace in a fixed order, so results stay deterministic (they may
+ * differ in the last bits from the NULL-workspace path). Contents need no
+ * initialisation and are not preserved; calls that can overlap in time must
+ * not share a workspace. A non-NULL workspace below the size is
+ * BMOE_ERR_WORKSPACE. The K loops are split only when whole tiles would leave
+ * the CUs idle for more than 48 K-steps (of 64 columns) on average; the
+ * environment variable BMOE_FFN_SPLIT_MIN_IDLE overrides that threshold.
  */
 BMOE_API bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
                              int32_t d_ff, const int32_t* offsets, const void* a,
                              const void* w_gate, const void* w_up, const void* w_down, void* h,
-                             void* y, void* stream);
+                             void* y, void* workspace, size_t workspace_bytes, void* stream);
 
 /* The two grouped GEMMs of brownout_moe_ffn, callable on their own (same
  * arguments and rules as brownout_moe_ffn):
@@ -191,10 +203,12 @@ BMOE_API bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows
  *   brownout_moe_ffn_down:    y = h W_down[s]^T                                   */
 BMOE_API bmoe_status brownout_moe_ffn_gate_up(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
                                      int32_t d_ff, const int32_t* offsets, const void* a,
-                                     const void* w_gate, const void* w_up, void* h, void* stream);
+                                     const void* w_gate, const void* w_up, void* h, void* workspace,
+                                     size_t workspace_bytes, void* stream);
 BMOE_API bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
                                   int32_t d_ff, const int32_t* offsets, const void* h,
-                                  const void* w_down, void* y, void* stream);
+                                  const void* w_down, void* y, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /*
  * brownout_moe_combine -- weighted sum back into token order (Sec. 2.1: the

@@ -84,11 +84,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_route.restype = I32
     lib.brownout_moe_dispatch.argtypes = [DP] + [P] * 8 + [SZ, P]
     lib.brownout_moe_dispatch.restype = I32
-    lib.brownout_moe_ffn.argtypes = [I32] * 5 + [P] * 8
+    lib.brownout_moe_ffn.argtypes = [I32] * 5 + [P] * 8 + [SZ, P]
     lib.brownout_moe_ffn.restype = I32
-    lib.brownout_moe_ffn_gate_up.argtypes = [I32] * 5 + [P] * 6
+    lib.brownout_moe_ffn_gate_up.argtypes = [I32] * 5 + [P] * 6 + [SZ, P]
     lib.brownout_moe_ffn_gate_up.restype = I32
-    lib.brownout_moe_ffn_down.argtypes = [I32] * 5 + [P] * 5
+    lib.brownout_moe_ffn_down.argtypes = [I32] * 5 + [P] * 5 + [SZ, P]
     lib.brownout_moe_ffn_down.restype = I32
     lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
     lib.brownout_moe_combine.restype = I32
@@ -202,6 +202,20 @@ def new_dispatch_workspace(desc: Desc, device) -> torch.Tensor:
     return torch.zeros((n + 255) // 256 * 256, dtype=torch.uint8, device=device)
 
 
+def new_ffn_workspace(desc: Desc, device) -> Optional[torch.Tensor]:
+    """The FFN stream-K workspace for this device (None when the layer has no
+    use for one: fp32, or no device)."""
+    n = workspace_bytes(desc, STAGE_FFN)
+    return torch.empty((n + 255) // 256 * 256, dtype=torch.uint8, device=device) if n else None
+
+
+def _ws(ws: Optional[torch.Tensor]):
+    if ws is None:
+        return None, 0
+    _dev(ws, "workspace", torch.uint8)
+    return _p(ws), ws.numel()
+
+
 def _ffn_checks(offsets, a_rows, dt, n_seg, d, d_ff):
     dtype = {torch.bfloat16: BMOE_BF16, torch.float32: BMOE_F32}.get(dt)
     if dtype is None:
@@ -212,8 +226,9 @@ def _ffn_checks(offsets, a_rows, dt, n_seg, d, d_ff):
 
 def ffn(offsets: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
         w_down: torch.Tensor, *, h: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
-        stream=None):
-    """Both grouped GEMMs: returns (y, h)."""
+        workspace: Optional[torch.Tensor] = None, stream=None):
+    """Both grouped GEMMs: returns (y, h). workspace: optional uint8 device
+    tensor of at least workspace_bytes(desc, STAGE_FFN) bytes (stream-K)."""
     n_seg, d_ff, d = w_gate.shape
     rows_cap, dt = a.shape[0], a.dtype
     dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
@@ -223,13 +238,14 @@ def ffn(offsets: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor, w_up: torc
     _dev(w_down, "w_down", dt, (n_seg, d, d_ff))
     h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
     y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, a.device)
+    wsp, wsn = _ws(workspace)
     st = load_library().brownout_moe_ffn(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a), _p(w_gate),
-                                         _p(w_up), _p(w_down), _p(h), _p(y), _stream(stream))
+                                         _p(w_up), _p(w_down), _p(h), _p(y), wsp, wsn, _stream(stream))
     _check(st, "brownout_moe_ffn")
     return y, h
 
 
-def ffn_gate_up(offsets, a, w_gate, w_up, *, h=None, stream=None):
+def ffn_gate_up(offsets, a, w_gate, w_up, *, h=None, workspace=None, stream=None):
     n_seg, d_ff, d = w_gate.shape
     rows_cap, dt = a.shape[0], a.dtype
     dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
@@ -237,21 +253,23 @@ def ffn_gate_up(offsets, a, w_gate, w_up, *, h=None, stream=None):
     _dev(w_gate, "w_gate", dt, (n_seg, d_ff, d))
     _dev(w_up, "w_up", dt, (n_seg, d_ff, d))
     h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
+    wsp, wsn = _ws(workspace)
     st = load_library().brownout_moe_ffn_gate_up(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a),
-                                                 _p(w_gate), _p(w_up), _p(h), _stream(stream))
+                                                 _p(w_gate), _p(w_up), _p(h), wsp, wsn, _stream(stream))
     _check(st, "brownout_moe_ffn_gate_up")
     return h
 
 
-def ffn_down(offsets, h, w_down, *, y=None, stream=None):
+def ffn_down(offsets, h, w_down, *, y=None, workspace=None, stream=None):
     n_seg, d, d_ff = w_down.shape
     rows_cap, dt = h.shape[0], h.dtype
     dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
     _dev(h, "h", dt, (rows_cap, d_ff))
     _dev(w_down, "w_down", dt, (n_seg, d, d_ff))
     y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, h.device)
+    wsp, wsn = _ws(workspace)
     st = load_library().brownout_moe_ffn_down(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(h),
-                                              _p(w_down), _p(y), _stream(stream))
+                                              _p(w_down), _p(y), wsp, wsn, _stream(stream))
     _check(st, "brownout_moe_ffn_down")
     return y
 
@@ -284,7 +302,7 @@ class LayerForward:
     [1,d_ff_shared,d], w_down_sh [1,d,d_ff_shared] (all device tensors).
     """
 
-    def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda"):
+    def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True):
         self.desc = desc
         self.w = weights
         _check(validate(desc), "bmoe_validate")
@@ -305,6 +323,7 @@ class LayerForward:
             "out": _empty((T, d), dt, device),
         }
         self.ws = new_dispatch_workspace(desc, device)
+        self.ffn_ws = new_ffn_workspace(desc, device) if stream_k else None
         if desc.d_ff_shared:
             self.bufs["h_sh"] = _empty((max(T, 1), desc.d_ff_shared), dt, device)
             self.bufs["y_sh"] = _empty((max(T, 1), d), dt, device)
@@ -322,21 +341,22 @@ class LayerForward:
     def ffn(self, stream=None):
         w = self.w
         return ffn(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
-                   w["w_up"], w["w_down"], h=self.bufs["h"], y=self.bufs["y"], stream=stream)
+                   w["w_up"], w["w_down"], h=self.bufs["h"], y=self.bufs["y"], workspace=self.ffn_ws,
+                   stream=stream)
 
     def ffn_gate_up(self, stream=None):
         w = self.w
         return ffn_gate_up(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
-                           w["w_up"], h=self.bufs["h"], stream=stream)
+                           w["w_up"], h=self.bufs["h"], workspace=self.ffn_ws, stream=stream)
 
     def ffn_down(self, stream=None):
         return ffn_down(self.bufs["dispatch"]["offsets"], self.bufs["h"], self.w["w_down"],
-                        y=self.bufs["y"], stream=stream)
+                        y=self.bufs["y"], workspace=self.ffn_ws, stream=stream)
 
     def shared(self, x, stream=None):
         w = self.w
         return ffn(self.sh_offsets, x, w["w_gate_sh"], w["w_up_sh"], w["w_down_sh"],
-                   h=self.bufs["h_sh"], y=self.bufs["y_sh"], stream=stream)
+                   h=self.bufs["h_sh"], y=self.bufs["y_sh"], workspace=self.ffn_ws, stream=stream)
 
     def combine(self, stream=None):
         y_sh = self.bufs["y_sh"] if self.desc.d_ff_shared else None

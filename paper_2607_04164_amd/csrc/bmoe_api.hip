@@ -60,6 +60,7 @@ bmoe_status bmoe_validate_map(const int32_t* e2g, int32_t E, int32_t G) {
 size_t bmoe_workspace_bytes(const bmoe_desc* d, int32_t stage) {
     if (bmoe_validate(d) != BMOE_OK) return 0;
     if (stage == BMOE_STAGE_DISPATCH) return dispatch_ws_bytes(d->T, d->G);
+    if (stage == BMOE_STAGE_FFN && d->dtype == BMOE_BF16) return ffn_workspace_bytes();
     return 0;
 }
 
@@ -101,7 +102,7 @@ namespace {
 
 bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
                        const int32_t* offsets, const void* a, const void* w_gate, const void* w_up,
-                       const void* w_down, void* h, void* y, void* stream) {
+                       const void* w_down, void* h, void* y, void* ws, size_t ws_bytes, void* stream) {
     if (dtype != BMOE_F32 && dtype != BMOE_BF16) return BMOE_ERR_UNSUPPORTED;
     if (n_seg < 1 || n_seg > BMOE_MAX_EXPERTS || rows_cap < 0) return BMOE_ERR_SHAPE;
     if (d < 8 || d % 8 != 0 || d_ff < 8 || d_ff % 8 != 0) return BMOE_ERR_SHAPE;
@@ -115,7 +116,10 @@ bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap,
     if (!aligned16(h)) return BMOE_ERR_ALIGN;
     if (up && (!aligned16(a) || !aligned16(w_gate) || !aligned16(w_up))) return BMOE_ERR_ALIGN;
     if (down && (!aligned16(w_down) || !aligned16(y))) return BMOE_ERR_ALIGN;
-    FfnArgs args{offsets, a, w_gate, w_up, w_down, h, y, n_seg, rows_cap, d, d_ff, dtype};
+    if (ws && ((uintptr_t)ws & 255u)) return BMOE_ERR_ALIGN;
+    if (dtype != BMOE_BF16) ws = nullptr;  // the fp32 kernels take no workspace
+    if (ws && ws_bytes < ffn_workspace_bytes()) return BMOE_ERR_WORKSPACE;
+    FfnArgs args{offsets, a, w_gate, w_up, w_down, h, y, ws, ws_bytes, n_seg, rows_cap, d, d_ff, dtype};
     return hip_status(launch_ffn(args, (hipStream_t)stream, part));
 }
 
@@ -125,24 +129,26 @@ extern "C" {
 
 bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
                              const int32_t* offsets, const void* a, const void* w_gate,
-                             const void* w_up, const void* w_down, void* h, void* y, void* stream) {
-    return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, stream);
+                             const void* w_up, const void* w_down, void* h, void* y, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+    return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, workspace,
+                      workspace_bytes, stream);
 }
 
 bmoe_status brownout_moe_ffn_gate_up(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
                                      int32_t d_ff, const int32_t* offsets, const void* a,
-                                     const void* w_gate, const void* w_up, void* h, void* stream) {
+                                     const void* w_gate, const void* w_up, void* h, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
     return ffn_common(1, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, nullptr, h, nullptr,
-                      stream);
+                      workspace, workspace_bytes, stream);
 }
 
 bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
                                   const int32_t* offsets, const void* h, const void* w_down, void* y,
-                                  void* stream) {
+                                  void* workspace, size_t workspace_bytes, void* stream) {
     // h is only read by the down GEMM
     return ffn_common(2, dtype, n_seg, rows_cap, d, d_ff, offsets, nullptr, nullptr, nullptr, w_down,
-                      const_cast<void*>(h), y,
-                      stream);
+                      const_cast<void*>(h), y, workspace, workspace_bytes, stream);
 }
 
 bmoe_status brownout_moe_combine(const bmoe_desc* d, const int32_t* slot_row, const float* slot_gate,

@@ -169,8 +169,12 @@ struct FfnArgs {
     const void* w_down;
     void* h;
     void* y;
+    void* ws;  // optional stream-K workspace (nullptr: one tile per workgroup)
+    size_t ws_bytes;
     int n_seg, rows_cap, d, d_ff, dtype;
 };
+// bytes of the stream-K workspace on the current device
+size_t ffn_workspace_bytes();
 // part: 0 = both GEMMs, 1 = gate/up only, 2 = down only
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part = 0);
 

@@ -19,6 +19,8 @@
 // past the real tile count exit at once.
 //
 // f32 path (small correctness configurations): one output element per thread.
+#include <cstdlib>
+
 #include "bmoe_common.h"
 
 namespace bmoe {
@@ -33,6 +35,7 @@ struct GemmParams {
     uint16_t* C;
     const int32_t* offsets;
     int n_seg, rows_cap, N, K;
+    int sk_min_idle;  // stream-K split threshold (average idle K-steps per workgroup)
 };
 
 template <bool GATED, int BM, int BN, int BK>
@@ -294,52 +297,57 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 // faster than 64-byte pieces; two 64 KB stages leave one stage in flight.
 // Measured on the grouped workloads, more stages of BK = 32 did not help:
 // the pipeline is bound by L2/MALL throughput, not by latency.
-#ifdef BMOE_FORCE_DMA_BK
-constexpr int kDmaBK = BMOE_FORCE_DMA_BK;
-#else
-constexpr int kDmaBK = 64;
-#endif
-#ifdef BMOE_FORCE_DMA_STAGES
-constexpr int kDmaStages = BMOE_FORCE_DMA_STAGES;
-#else
-constexpr int kDmaStages = 2;
-#endif
+// ---- bf16 grouped GEMM with direct-to-LDS copies (large groups)
+//
+// 256x256 workgroup tile (gate/up: 128 columns of each of W_gate and W_up, so
+// SiLU(gate)*up happens in the epilogue), 128x128 per wave, 32x32x16 bf16 MFMA
+// with fp32 accumulators, K-step 64 through a two-slot LDS ring filled by
+// global_load_lds_dwordx4.
+//
+// Work distribution. Without a workspace every workgroup computes one tile.
+// With one (stream-K), the grid is one workgroup per CU: full rounds of one
+// tile per workgroup, then the K-steps of the remaining tiles (between one
+// and two rounds' worth) are split evenly across the workgroups. A workgroup
+// whose share starts or ends inside a tile writes that piece's fp32
+// accumulators to its workspace slot, and a second kernel sums the pieces of
+// each split tile in K order and applies the epilogue. No workgroup ever
+// waits for another, so nothing depends on which workgroups are resident.
+
 #ifdef BMOE_FORCE_GROUP_M
 constexpr int kGroupM = BMOE_FORCE_GROUP_M;
 #else
 constexpr int kGroupM = 4;
 #endif
+constexpr int kDmaBK = 64;
+constexpr int kSkPartBytes = 256 * 256 * 4;  // fp32 accumulators of one tile piece
 
-
-template <bool GATED, int NSTAGE, int BKV>
+template <bool GATED>
 struct DmaCfg {
-    static constexpr int BM = 256, BK = BKV, STAGES = NSTAGE, KC = BK / 8;  // KC: 16-byte chunks per row
-    static constexpr int SUB = BK / 16;                                      // MFMA sub-steps per stage
-    static constexpr int BN = GATED ? 128 : 256;  // output columns per matrix
+    static constexpr int BM = 256, BK = kDmaBK, KC = BK / 8;  // KC: 16-byte chunks per row
+    static constexpr int SUB = BK / 16;                       // MFMA sub-steps per K-step
+    static constexpr int BN = GATED ? 128 : 256;              // output columns per matrix
     static constexpr int NMAT = GATED ? 2 : 1;
-    static constexpr int RB = NMAT * BN;          // B rows staged per K-step (256)
+    static constexpr int RB = NMAT * BN;                      // B rows staged per K-step (256)
     static constexpr int WTM = BM / 2, WTN = BN / 2;
     static constexpr int MB = WTM / 32, NB = WTN / 32;
     static constexpr int ROW_BYTES = BK * 2;
-    static constexpr int ROWS_PER_DMA = 64 / KC;                   // rows one DMA instruction fills
-    static constexpr int A_DMA = BM / (4 * ROWS_PER_DMA);          // per wave per stage
+    static constexpr int ROWS_PER_DMA = 64 / KC;              // rows one DMA instruction fills
+    static constexpr int A_DMA = BM / (4 * ROWS_PER_DMA);     // per wave per K-step
     static constexpr int B_DMA = RB / (4 * ROWS_PER_DMA);
     static constexpr int DMA_PER_STAGE = A_DMA + B_DMA;
     static constexpr int A_STAGE = BM * ROW_BYTES, B_STAGE = RB * ROW_BYTES;
     static constexpr int STAGE = A_STAGE + B_STAGE;
     static constexpr int SROW = WTN + 8;
     static constexpr int EPI = 4 * WTM * SROW * 2;
-    static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;  // tile-schedule arrays
-    // NSTAGE == 5 selects the unit ring: five 32 KB slots that each hold the A
-    // half or the B half of a K-step (units A0 B0 A1 B1 ..., unit u in slot
-    // u % 5), so one and a half K-steps are in flight while one is read
-    static constexpr bool UNITS = NSTAGE == 5;
-    static constexpr int RING = UNITS ? 5 * A_STAGE : STAGES * STAGE;
-    static constexpr int SMEM = (RING > EPI ? RING : EPI) > SCHED ? (RING > EPI ? RING : EPI) : SCHED;
-    static_assert((KC == 4 || KC == 8) && BM == 256 && RB == 256, "tile shape");
-    static_assert(SUB % 2 == 0, "fragment double buffer alternates within a stage");
+    static constexpr int RING = 2 * STAGE;
+    static constexpr int SCHED_OFF = RING > EPI ? RING : EPI;             // schedule arrays live after
+    static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;   // the ring / staging area
+    static constexpr int SMEM = SCHED_OFF + SCHED;
+    static constexpr int NACC4 = NMAT * MB * NB * 4;                      // float4 accumulators per lane
+    static_assert(KC == 8 && BM == 256 && RB == 256, "tile shape");
+    static_assert(SUB % 2 == 0, "fragment double buffer alternates within a K-step");
     static_assert(SMEM <= 160 * 1024, "LDS of one workgroup");
-    static_assert(!UNITS || (A_STAGE == B_STAGE && A_DMA == B_DMA), "units of equal size");
+    static_assert(NACC4 * 16 * kGemmThreads == kSkPartBytes, "piece size");
 };
 
 // 16-byte chunk swizzle of a tile row: conflict-free 128-bit fragment reads
@@ -360,7 +368,7 @@ struct DmaSrc {
     uint32_t b_off[C::B_DMA];
 };
 
-// DMA instruction i of the wave's share of a stage: instructions 0..A_DMA-1
+// DMA instruction i of the wave's share of a K-step: instructions 0..A_DMA-1
 // fill A rows, the rest B rows; instruction i of wave w fills ROWS_PER_DMA
 // consecutive rows (1 KB of LDS). kb: byte offset of the K-step in a row.
 template <class C>
@@ -395,65 +403,6 @@ __device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMA
             bf[mat][nb] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
 }
 
-template <class C>
-__device__ __forceinline__ void dma_mfmas(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                          const uint4 (&bf)[C::NMAT][C::NB]) {
-#pragma unroll
-    for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < C::NB; ++nb) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
-}
-
-// DMA instruction i of the wave's share of unit u (u even: A half of K-step
-// u/2, u odd: B half) into the slot at slot_lds.
-template <class C>
-__device__ __forceinline__ void dma_unit_one(const DmaSrc<C>& src, uint32_t slot_lds, int wave, int u, int i) {
-    const int kb = (u >> 1) * C::BK * 2;
-    if ((u & 1) == 0)
-        dma16s(src.a_base + kb, src.a_off[i], slot_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
-    else
-        dma16s(src.b_base + kb, src.b_off[i], slot_lds + ((wave * C::B_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
-}
-
-template <class C>
-__device__ __forceinline__ void dma_frags_ab(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB], const char* a_slot,
-                                             const char* b_slot, int wm, int wn, int lane, int kk) {
-    const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
-        af[mb] = *(const uint4*)(a_slot + lds_off<C>(wm * C::WTM + mb * 32 + l32, c));
-#pragma unroll
-    for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-        for (int nb = 0; nb < C::NB; ++nb)
-            bf[mat][nb] = *(const uint4*)(b_slot + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
-}
-
-// The MFMAs of one sub-step with the copies of units u0 and u1 (one copy
-// instruction after each MFMA; only the asm copy sits behind a branch).
-template <class C>
-__device__ __forceinline__ void unit_mfmas_ilv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                               const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
-                                               uint32_t lds0, int wave, int u0, int u1, int nu) {
-    constexpr int NM = C::NMAT * C::MB * C::NB;
-    static_assert(2 * C::A_DMA == NM, "one copy per MFMA");
-    const uint32_t s0 = lds0 + (u0 % 5) * C::A_STAGE, s1 = lds0 + (u1 % 5) * C::A_STAGE;
-#pragma unroll
-    for (int q = 0; q < NM; ++q) {
-        const int mat = q / (C::MB * C::NB), mb = (q / C::NB) % C::MB, nb = q % C::NB;
-        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
-        __builtin_amdgcn_sched_barrier(0);
-        if (q < C::A_DMA) {
-            if (u0 < nu) dma_unit_one<C>(src, s0, wave, u0, q);
-        } else {
-            if (u1 < nu) dma_unit_one<C>(src, s1, wave, u1, q - C::A_DMA);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-}
-
 // The MFMAs of one sub-step (A-fragment-major order) with the fragment reads
 // of the next sub-step spread between them, one read after every second
 // MFMA, in the order the next sub-step consumes them (all B fragments, then
@@ -461,8 +410,8 @@ __device__ __forceinline__ void unit_mfmas_ilv(f32x16 (&acc)[C::NMAT][C::MB][C::
 template <class C>
 __device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
                                                  const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga)[C::MB],
-                                                 uint4 (&gb)[C::NMAT][C::NB], const char* a_slot,
-                                                 const char* b_slot, int wm, int wn, int lane, int kk) {
+                                                 uint4 (&gb)[C::NMAT][C::NB], const char* stage, int wm, int wn,
+                                                 int lane, int kk) {
     constexpr int NM = C::NMAT * C::MB * C::NB, NR = C::MB + C::NMAT * C::NB;
     static_assert(2 * NR == NM, "one read per two MFMAs");
     const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
@@ -475,119 +424,184 @@ __device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C
             __builtin_amdgcn_sched_barrier(0);
             if (r < C::NMAT * C::NB) {
                 const int rm = r / C::NB, rn = r % C::NB;
-                gb[rm][rn] = *(const uint4*)(b_slot + lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
+                gb[rm][rn] = *(const uint4*)(stage + C::A_STAGE +
+                                             lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
             } else {
                 const int ra = r - C::NMAT * C::NB;
-                ga[ra] = *(const uint4*)(a_slot + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
+                ga[ra] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
             }
             __builtin_amdgcn_sched_barrier(0);
         }
     }
 }
 
-// The MFMAs of one sub-step with the wave's DMA instructions of a stage
+// The MFMAs of one sub-step with the wave's DMA instructions of a K-step
 // spread between them, so that a DMA issue that waits for queue space does
-// not hold back a run of MFMAs.
+// not hold back a run of MFMAs. Only the asm copy sits behind the (uniform)
+// branch: MFMAs under control flow make the compiler shuffle accumulators.
 template <class C>
-__device__ __forceinline__ void dma_mfmas_ilv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                              const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
-                                              uint32_t stage_lds, int wave, int kb, bool do_dma) {
+__device__ __forceinline__ void mfmas_with_dma(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                               const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
+                                               uint32_t stage_lds, int wave, int kb, bool do_dma) {
     constexpr int NM = C::NMAT * C::MB * C::NB;
-    static_assert(C::DMA_PER_STAGE <= NM, "one DMA per MFMA at most");
+    static_assert(C::DMA_PER_STAGE == NM, "one DMA per MFMA");
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
-        const int mat = q / (C::MB * C::NB), mb = (q / C::NB) % C::MB, nb = q % C::NB;
+        const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
         acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
-        if (q * C::DMA_PER_STAGE % NM < C::DMA_PER_STAGE) {
-            // only the asm copy sits behind the (uniform) branch: MFMAs under
-            // control flow make the compiler shuffle the accumulators
-            __builtin_amdgcn_sched_barrier(0);
-            if (do_dma) dma_one<C>(src, stage_lds, wave, kb, q * C::DMA_PER_STAGE / NM);
-            __builtin_amdgcn_sched_barrier(0);
-        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (do_dma) dma_one<C>(src, stage_lds, wave, kb, q);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
-template <bool GATED, int NSTAGE, int BKV>
-__global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmParams p) {
-    using C = DmaCfg<GATED, NSTAGE, BKV>;
-    constexpr int BM = C::BM, BN = C::BN;
-    __shared__ __align__(16) char smem[C::SMEM];
-    // the tile-schedule arrays live in the first bytes of the ring; they are
-    // dead (copied to registers, then a barrier) before the first DMA
-    int* s_scan = (int*)smem;
-    int* s_mt = s_scan + 256;
-    int* s_beg = s_mt + BMOE_MAX_EXPERTS + 1;
-    int* s_end = s_beg + BMOE_MAX_EXPERTS;
+// ---- tile schedule: per-segment M-tile prefix in LDS, computed from the
+// device offsets by every workgroup (the host does not read the offsets)
+struct TileSched {
+    int* s_mt;   // [n_seg + 1] first M-tile of each segment
+    int* s_beg;  // [n_seg] first row of each segment
+    int* s_end;  // [n_seg] end row of each segment
+    int NT, total_mt;
+};
 
-    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-    const int n_seg = p.n_seg, N = p.N, K = p.K;
+struct TileCoord {
+    int s, m0, m_end, n0;
+};
 
-    // ---- tile schedule from the device offsets (same mapping as the other GEMMs)
+// Returns the schedule; ends with a barrier. The arrays must not be written
+// while a workgroup uses them (they live outside the ring and staging area).
+__device__ __forceinline__ TileSched tile_sched(const GemmParams& p, char* sched_lds, int BM, int BN) {
+    TileSched t;
+    int* s_scan = (int*)sched_lds;
+    t.s_mt = s_scan + 256;
+    t.s_beg = t.s_mt + BMOE_MAX_EXPERTS + 1;
+    t.s_end = t.s_beg + BMOE_MAX_EXPERTS;
+    const int tid = threadIdx.x;
     int cnt = 0;
-    if (tid < n_seg) {
-        int beg = min(max(p.offsets[tid], 0), p.rows_cap);
-        int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
-        s_beg[tid] = beg;
-        s_end[tid] = end;
+    if (tid < p.n_seg) {
+        const int beg = min(max(p.offsets[tid], 0), p.rows_cap);
+        const int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
+        t.s_beg[tid] = beg;
+        t.s_end[tid] = end;
         cnt = ceil_div(end - beg, BM);
     }
     int total_mt;
     const int ex = block_exclusive_scan_256(cnt, s_scan, &total_mt);
-    if (tid < n_seg) s_mt[tid] = ex;
-    if (tid == 0) s_mt[n_seg] = total_mt;
+    if (tid < p.n_seg) t.s_mt[tid] = ex;
+    if (tid == 0) t.s_mt[p.n_seg] = total_mt;
     __syncthreads();
-    const int NT = ceil_div(N, BN);
-    const int L = xcd_swizzle(blockIdx.x, gridDim.x);
-    if (L >= total_mt * NT) return;
+    t.total_mt = __builtin_amdgcn_readfirstlane(total_mt);
+    t.NT = ceil_div(p.N, BN);
+    return t;
+}
+
+// Tile L of the schedule: segments in order; inside a segment, groups of
+// kGroupM M-tiles with N-tiles outer, so that the workgroups that run
+// together on one XCD share A and B panels in L2. The values come from LDS;
+// readfirstlane keeps them (and the copy bases) in SGPRs.
+__device__ __forceinline__ TileCoord tile_coord(const TileSched& t, int n_seg, int L, int BM, int BN) {
+    const int NT = t.NT;
     int lo = 0, hi = n_seg - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (s_mt[mid] * NT <= L) lo = mid;
+        if (t.s_mt[mid] * NT <= L) lo = mid;
         else hi = mid - 1;
     }
-    // the schedule values come from LDS; they are workgroup-uniform, and
-    // readfirstlane lets the compiler keep them (and the copy bases) in SGPRs
-    const int s = __builtin_amdgcn_readfirstlane(lo);
-    const int mts = __builtin_amdgcn_readfirstlane(s_mt[s + 1] - s_mt[s]);
-    const int local = L - __builtin_amdgcn_readfirstlane(s_mt[s]) * NT;
-    // tiles of a segment in groups of kGroupM M-tiles, N-tiles outer within a
-    // group: the workgroups that run together on one XCD share A and B panels
+    TileCoord c;
+    c.s = __builtin_amdgcn_readfirstlane(lo);
+    const int mts = __builtin_amdgcn_readfirstlane(t.s_mt[c.s + 1] - t.s_mt[c.s]);
+    const int local = L - __builtin_amdgcn_readfirstlane(t.s_mt[c.s]) * NT;
     const int mg = local / (kGroupM * NT), gm = min(kGroupM, mts - mg * kGroupM);
     const int rem = local - mg * kGroupM * NT;
     const int nt = rem / gm, mt = mg * kGroupM + rem % gm;
-    const int m0 = __builtin_amdgcn_readfirstlane(s_beg[s]) + mt * BM;
-    const int m_end = __builtin_amdgcn_readfirstlane(s_end[s]);
-    const int n0 = nt * BN;
-    __syncthreads();  // schedule arrays are overwritten by the first DMAs
+    c.m0 = __builtin_amdgcn_readfirstlane(t.s_beg[c.s]) + mt * BM;
+    c.m_end = __builtin_amdgcn_readfirstlane(t.s_end[c.s]);
+    c.n0 = nt * BN;
+    return c;
+}
 
-    // ---- per-lane DMA sources: lane l of instruction i of wave w fills LDS row
-    // r = (w*N_DMA + i)*ROWS_PER_DMA + l/KC, physical chunk l%KC, i.e. logical
-    // chunk (l%KC) ^ swz(r); the KC lanes of a row read its contiguous bytes
-    DmaSrc<C> src;
+template <class C, bool GATED>
+__device__ __forceinline__ void dma_sources(DmaSrc<C>& src, const GemmParams& p, const TileCoord& tc, int wave,
+                                            int lane) {
+    const int K = p.K, N = p.N;
     const int lrow = lane / C::KC, lchk = lane % C::KC;
-    src.a_base = (const char*)(p.A + (size_t)m0 * K);
+    src.a_base = (const char*)(p.A + (size_t)tc.m0 * K);
 #pragma unroll
     for (int i = 0; i < C::A_DMA; ++i) {
         const int r = (wave * C::A_DMA + i) * C::ROWS_PER_DMA + lrow;
-        const int row = min(m0 + r, m_end - 1);
-        src.a_off[i] = (uint32_t)(((row - m0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
+        const int row = min(tc.m0 + r, tc.m_end - 1);
+        src.a_off[i] = (uint32_t)(((row - tc.m0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
     // a wave's B rows lie in one matrix (gate or up for the gated GEMM)
-    static_assert(!GATED || (C::B_DMA * C::ROWS_PER_DMA * 2 == BN), "B rows of a wave in one matrix");
-    const int bmat = GATED ? (wave * C::B_DMA * C::ROWS_PER_DMA) / BN : 0;
-    src.b_base = (const char*)((bmat ? p.B1 : p.B0) + ((size_t)s * N + n0) * K);
+    static_assert(!GATED || (C::B_DMA * C::ROWS_PER_DMA * 2 == C::BN), "B rows of a wave in one matrix");
+    const int bmat = GATED ? (wave * C::B_DMA * C::ROWS_PER_DMA) / C::BN : 0;
+    src.b_base = (const char*)((bmat ? p.B1 : p.B0) + ((size_t)tc.s * N + tc.n0) * K);
 #pragma unroll
     for (int i = 0; i < C::B_DMA; ++i) {
         const int r = (wave * C::B_DMA + i) * C::ROWS_PER_DMA + lrow;
-        const int n = min(n0 + r % BN, N - 1);
-        src.b_off[i] = (uint32_t)(((n - n0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
+        const int n = min(tc.n0 + r % C::BN, N - 1);
+        src.b_off[i] = (uint32_t)(((n - tc.n0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
+}
+
+// K-steps [ka, kb) of one tile into acc (which the caller zeroed). Ends with
+// every copy complete and a barrier, so the LDS may be reused.
+template <class C>
+__device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
+                                            char* smem, int ka, int kb, int wave, int lane) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
     const int wm = wave >> 1, wn = wave & 1;
-    const int nk = K / C::BK;
+    const int n = kb - ka;
+    // prologue: K-steps ka and ka+1 in flight, wait for ka
+    dma_stage<C>(src, lds0, wave, ka * C::BK * 2);
+    if (n > 1) dma_stage<C>(src, lds0 + C::STAGE, wave, (ka + 1) * C::BK * 2);
+    if (n > 1) wait_vmcnt<C::DMA_PER_STAGE>();
+    else wait_vmcnt<0>();
+    wg_barrier();
+    uint4 af0[C::MB], af1[C::MB];
+    uint4 bf0[C::NMAT][C::NB], bf1[C::NMAT][C::NB];
+    dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
 
-    f32x16 acc[C::NMAT][C::MB][C::NB];
+    // The LDS reads of every K-step are unconditional (the last step reads a
+    // stale slot and drops it), so the compiler's LDS wait counts never merge
+    // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
+    // sched_barrier(0) fences keep each group of fragment reads ahead of the
+    // MFMA group that hides its latency.
+    for (int kt = 0; kt < n; ++kt) {
+        const int slot = kt & 1;
+        const char* stage = smem + slot * C::STAGE;
+#pragma unroll
+        for (int j = 0; j < C::SUB; ++j) {
+            uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
+            uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
+            uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
+            uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
+            __builtin_amdgcn_sched_barrier(0);
+            // the last sub-step carries the copies of K-step kt+2 (its slot was
+            // released by the barrier of the previous sub-step); the others
+            // carry the fragment reads of the next sub-step
+            if (j == C::SUB - 1)  // resolved by the unrolling
+                mfmas_with_dma<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (ka + kt + 2) * C::BK * 2,
+                                  kt + 2 < n);
+            else
+                mfmas_with_reads<C>(acc, fa, fb, ga, gb, stage, wm, wn, lane, j + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (j == C::SUB - 2) {
+                // copies issued so far: K-steps up to min(n-1, kt+1); kt+1 must be resident
+                if (kt + 1 < n) wait_vmcnt<0>();
+                lds_reads_done();
+                wg_barrier();
+                // registers of this sub-step are free now: next K-step, sub-step 0
+                dma_frags<C>(fa, fb, smem + (slot ^ 1) * C::STAGE, wm, wn, lane, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+    __syncthreads();
+}
+
+template <class C>
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[C::NMAT][C::MB][C::NB]) {
 #pragma unroll
     for (int mat = 0; mat < C::NMAT; ++mat)
 #pragma unroll
@@ -596,104 +610,14 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             for (int nb = 0; nb < C::NB; ++nb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) acc[mat][mb][nb][i] = 0.f;
+}
 
-    uint4 af0[C::MB], af1[C::MB];
-    uint4 bf0[C::NMAT][C::NB], bf1[C::NMAT][C::NB];
-    if constexpr (C::UNITS) {
-        // ---- unit ring: units 0..4 in flight, wait for units 0 and 1
-        const int nu = 2 * nk;
-#pragma unroll
-        for (int u = 0; u < 5; ++u)
-            if (u < nu)
-#pragma unroll
-                for (int i = 0; i < C::A_DMA; ++i) dma_unit_one<C>(src, lds0 + u * C::A_STAGE, wave, u, i);
-        wait_vmcnt_rt<C::A_DMA>(min(nu, 5) - 2);
-        wg_barrier();
-        dma_frags_ab<C>(af0, bf0, smem, smem + C::A_STAGE, wm, wn, lane, 0);
-        int ua = 0;  // slot of unit 2*kt (A half of the current K-step)
-        for (int kt = 0; kt < nk; ++kt) {
-            const int ub = ua == 4 ? 0 : ua + 1;
-            const int na = ub == 4 ? 0 : ub + 1, nb2 = na == 4 ? 0 : na + 1;
-            const char* a_slot = smem + ua * C::A_STAGE;
-            const char* b_slot = smem + ub * C::A_STAGE;
-#pragma unroll
-            for (int j = 0; j < C::SUB; ++j) {
-                uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
-                uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
-                uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
-                uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
-                if (j + 1 < C::SUB) dma_frags_ab<C>(ga, gb, a_slot, b_slot, wm, wn, lane, j + 1);
-                __builtin_amdgcn_sched_barrier(0);
-                // the last sub-step carries units 2kt+5 and 2kt+6, whose slots
-                // (those of the current K-step) the barrier below released
-                if (j == C::SUB - 1)  // resolved by the unrolling
-                    unit_mfmas_ilv<C>(acc, fa, fb, src, lds0, wave, 2 * kt + 5, 2 * kt + 6, nu);
-                else
-                    dma_mfmas<C>(acc, fa, fb);
-                __builtin_amdgcn_sched_barrier(0);
-                if (j == C::SUB - 2) {
-                    // units issued so far: 0 .. min(nu, 2kt+5)-1; units 2kt+2
-                    // and 2kt+3 (next K-step) must be resident
-                    wait_vmcnt_rt<C::A_DMA>(max(0, min(nu, 2 * kt + 5) - (2 * kt + 4)));
-                    lds_reads_done();
-                    wg_barrier();
-                    dma_frags_ab<C>(fa, fb, smem + na * C::A_STAGE, smem + nb2 * C::A_STAGE, wm, wn, lane, 0);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            }
-            ua = na;
-        }
-    } else {
-        // ---- prologue: the first STAGES stages in flight, wait for stage 0
-#pragma unroll
-        for (int st = 0; st < C::STAGES; ++st)
-            if (st < nk) dma_stage<C>(src, lds0 + st * C::STAGE, wave, st * C::BK * 2);
-        wait_vmcnt_rt<C::DMA_PER_STAGE>(min(nk, C::STAGES) - 1);
-        wg_barrier();
-        dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
-
-        // The LDS reads of every K-step are unconditional (the last step reads a
-        // stale slot and drops it), so the compiler's LDS wait counts never merge
-        // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
-        // sched_barrier(0) fences keep each group of fragment reads ahead of the
-        // MFMA group that hides its latency (the scheduler would otherwise sink
-        // the next stage's reads to the top of the next iteration).
-        int slot = 0;
-        for (int kt = 0; kt < nk; ++kt) {
-            const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
-            const char* stage = smem + slot * C::STAGE;
-#pragma unroll
-            for (int j = 0; j < C::SUB; ++j) {
-                uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
-                uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
-                uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
-                uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
-                __builtin_amdgcn_sched_barrier(0);
-                // the last sub-step carries the DMAs of stage kt+STAGES (its slot
-                // was released by the barrier of the previous sub-step); the
-                // others carry the fragment reads of the next sub-step
-                if (j == C::SUB - 1)  // resolved by the unrolling
-                    dma_mfmas_ilv<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (kt + C::STAGES) * C::BK * 2,
-                                     kt + C::STAGES < nk);
-                else
-                    mfmas_with_reads<C>(acc, fa, fb, ga, gb, stage, stage + C::A_STAGE, wm, wn, lane, j + 1);
-                __builtin_amdgcn_sched_barrier(0);
-                if (j == C::SUB - 2) {
-                    // stages issued so far: 0 .. min(nk-1, kt+STAGES-1); stage kt+1 must be resident
-                    wait_vmcnt_rt<C::DMA_PER_STAGE>(max(0, min(nk - 1, kt + C::STAGES - 1) - (kt + 1)));
-                    lds_reads_done();
-                    wg_barrier();
-                    // registers of this sub-step are free now: next stage, sub-step 0
-                    dma_frags<C>(fa, fb, smem + next * C::STAGE, wm, wn, lane, 0);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            }
-            slot = next;
-        }
-    }
-    __syncthreads();
-
-    // ---- epilogue: stage the wave's tile in LDS, then 128-bit row stores
+// Epilogue: the wave's tile (SiLU(gate)*up for the gated GEMM) is staged in
+// LDS as bf16, then written with 128-bit row stores. Ends with a barrier.
+template <class C, bool GATED>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], const GemmParams& p,
+                                           const TileCoord& tc, char* smem, int wave, int lane) {
+    const int wm = wave >> 1, wn = wave & 1;
     uint16_t* st = (uint16_t*)smem + (size_t)wave * C::WTM * C::SROW;
     const int l32 = lane & 31;
 #pragma unroll
@@ -718,25 +642,207 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             }
     __syncthreads();
     constexpr int CPR = C::WTN / 8;
-    const int row0 = m0 + wm * C::WTM, col0 = n0 + wn * C::WTN;
+    const int row0 = tc.m0 + wm * C::WTM, col0 = tc.n0 + wn * C::WTN;
 #pragma unroll 4
     for (int c = lane; c < C::WTM * CPR; c += 64) {
         const int r = c / CPR, cc = c % CPR;
         const int gm = row0 + r, gn = col0 + cc * 8;
-        if (gm < m_end && gn < N)
-            *(uint4*)(p.C + (size_t)gm * N + gn) = *(const uint4*)(st + r * C::SROW + cc * 8);
+        if (gm < tc.m_end && gn < p.N)
+            *(uint4*)(p.C + (size_t)gm * p.N + gn) = *(const uint4*)(st + r * C::SROW + cc * 8);
+    }
+    __syncthreads();
+}
+
+// fp32 accumulators of a tile piece, lane-interleaved float4 (coalesced)
+template <class C>
+__device__ __forceinline__ void store_piece(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], char* slot) {
+    float4* d = (float4*)slot;
+    int q = 0;
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 16; i += 4, ++q)
+                    d[q * kGemmThreads + threadIdx.x] =
+                        make_float4(acc[mat][mb][nb][i], acc[mat][mb][nb][i + 1], acc[mat][mb][nb][i + 2],
+                                    acc[mat][mb][nb][i + 3]);
+}
+
+template <class C>
+__device__ __forceinline__ void add_piece(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const char* slot) {
+    const float4* d = (const float4*)slot;
+    int q = 0;
+#pragma unroll
+    for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 16; i += 4, ++q) {
+                    const float4 v = d[q * kGemmThreads + threadIdx.x];
+                    acc[mat][mb][nb][i] += v.x;
+                    acc[mat][mb][nb][i + 1] += v.y;
+                    acc[mat][mb][nb][i + 2] += v.z;
+                    acc[mat][mb][nb][i + 3] += v.w;
+                }
+}
+
+// Work of P persistent workgroups: F rounds of one tile each (round r, tile
+// r*P + w; the last round may be partial), then, split by K-steps, the tiles
+// [F*P, total): each workgroup gets `share` consecutive K-steps of those.
+// The split moves two fp32 tile pieces per workgroup through memory and
+// restarts the pipeline per piece, so it is used (with a workspace) only when
+// whole tiles would leave the workgroups idle for more than min_idle K-steps
+// on average (kSkMinIdle unless BMOE_FFN_SPLIT_MIN_IDLE says otherwise).
+constexpr int kSkMinIdle = 48;
+struct SkSplit {
+    int F, W, share;
+};
+__device__ __forceinline__ SkSplit sk_split(int total, int nk, int P, bool can_split, int min_idle) {
+    SkSplit k;
+    const int rounds = ceil_div(total, P);
+    const int64_t idle = (int64_t)(rounds * P - total) * nk;  // K-steps, summed over workgroups
+    if (!can_split || total == 0 || idle <= (int64_t)min_idle * P) {
+        k.F = rounds;
+        k.W = 0;
+        k.share = 1;
+    } else {
+        k.F = max(0, total / P - 1);
+        k.W = (total - k.F * P) * nk;
+        k.share = ceil_div(k.W, P);
+    }
+    return k;
+}
+
+template <bool GATED, bool SK>
+__global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmParams p, char* ws) {
+    using C = DmaCfg<GATED>;
+    __shared__ __align__(16) char smem[C::SMEM];
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const TileSched ts = tile_sched(p, smem + C::SCHED_OFF, C::BM, C::BN);
+    const int total = ts.total_mt * ts.NT;
+    const int nk = p.K / C::BK;
+    f32x16 acc[C::NMAT][C::MB][C::NB];
+    DmaSrc<C> src;
+    if constexpr (!SK) {
+        const int L = xcd_swizzle(blockIdx.x, gridDim.x);
+        if (L >= total) return;
+        const TileCoord tc = tile_coord(ts, p.n_seg, L, C::BM, C::BN);
+        dma_sources<C, GATED>(src, p, tc, wave, lane);
+        zero_acc<C>(acc);
+        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane);
+        store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
+    } else {
+        const int P = gridDim.x;
+        const int pw = xcd_swizzle(blockIdx.x, P);
+        const SkSplit sk = sk_split(total, nk, P, ws != nullptr, p.sk_min_idle);
+        // work items: full rounds (one tile each), then this workgroup's share
+        // of the remaining K-steps; one loop so every stage is inlined once
+        const int i0 = min(sk.W, pw * sk.share), i1 = min(sk.W, i0 + sk.share);
+        int r = 0, i = i0;
+        while (true) {
+            int L, ka, kb, slot = -1;
+            if (r < sk.F) {
+                L = r * P + pw;
+                ka = 0;
+                kb = nk;
+                ++r;
+                if (L >= total) continue;  // last whole-tile round is partial
+            } else if (i < i1) {
+                const int t = i / nk;
+                ka = i - t * nk;
+                kb = min(nk, ka + (i1 - i));
+                L = sk.F * P + t;
+                // slot 0: the piece that starts the share, slot 1: the one that ends it
+                if (ka != 0 || kb != nk) slot = i == i0 ? 0 : 1;
+                i += kb - ka;
+            } else {
+                break;
+            }
+            const TileCoord tc = tile_coord(ts, p.n_seg, L, C::BM, C::BN);
+            dma_sources<C, GATED>(src, p, tc, wave, lane);
+            zero_acc<C>(acc);
+            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane);
+            if (slot < 0) store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
+            else store_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkPartBytes);
+        }
     }
 }
 
+// Sums the pieces of every tile that the stream-K split cut, in K order,
+// then applies the epilogue. Workgroup b looks at the share boundary b*share;
+// the first boundary inside a tile owns that tile.
 template <bool GATED>
-hipError_t launch_gemm_dma(const GemmParams& g, hipStream_t s) {
-    using C = DmaCfg<GATED, kDmaStages, kDmaBK>;
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_fixup_kernel(GemmParams p, const char* ws, int P) {
+    using C = DmaCfg<GATED>;
+    __shared__ __align__(16) char smem[C::SMEM];
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int b = blockIdx.x;
+    if (b == 0) return;
+    const TileSched ts = tile_sched(p, smem + C::SCHED_OFF, C::BM, C::BN);
+    const int nk = p.K / C::BK;
+    const SkSplit sk = sk_split(ts.total_mt * ts.NT, nk, P, true, p.sk_min_idle);
+    const int q = b * sk.share;
+    if (q >= sk.W || q % nk == 0) return;
+    const int t = q / nk;
+    if (b != t * nk / sk.share + 1) return;  // not the first boundary inside tile t
+    const int p0 = t * nk / sk.share, p1 = ((t + 1) * nk - 1) / sk.share;
+    f32x16 acc[C::NMAT][C::MB][C::NB];
+    zero_acc<C>(acc);
+    for (int pw = p0; pw <= p1; ++pw) {
+        const int slot = pw * sk.share >= t * nk ? 0 : 1;  // share starts inside tile t, or ends in it
+        add_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkPartBytes);
+    }
+    const TileCoord tc = tile_coord(ts, p.n_seg, sk.F * P + t, C::BM, C::BN);
+    store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
+}
+
+// CUs of the current device, rounded down to a multiple of 8 (XCD deal)
+static int stream_k_workgroups() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cached[dev] = n / 8 * 8;
+    }
+    return cached[dev];
+}
+
+static int split_min_idle() {
+    const char* e = getenv("BMOE_FFN_SPLIT_MIN_IDLE");
+    if (e == nullptr || *e == 0) return kSkMinIdle;
+    const long v = strtol(e, nullptr, 10);
+    return v < 0 ? 0 : (v > (1 << 20) ? (1 << 20) : (int)v);
+}
+
+template <bool GATED>
+hipError_t launch_gemm_dma(const GemmParams& g0, void* ws, size_t ws_bytes, hipStream_t s) {
+    using C = DmaCfg<GATED>;
+    GemmParams g = g0;
+    g.sk_min_idle = split_min_idle();
+    // persistent: one workgroup per CU, each XCD a contiguous range of tiles
+    const int P = stream_k_workgroups();
+    if (P > 0) {
+        const bool split = ws != nullptr && ws_bytes >= (size_t)2 * P * kSkPartBytes;
+        hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, true>), dim3(P), dim3(kGemmThreads), 0, s, g,
+                           split ? (char*)ws : (char*)nullptr);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || !split) return e;
+        hipLaunchKernelGGL((gemm_fixup_kernel<GATED>), dim3(P), dim3(kGemmThreads), 0, s, g, (const char*)ws, P);
+        return hipGetLastError();
+    }
     const int64_t mt_max = ceil_div64(g.rows_cap, C::BM) + g.n_seg;
     const int64_t nt = ceil_div64(g.N, C::BN);
     int64_t blocks = (mt_max * nt + 7) / 8 * 8;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, kDmaStages, kDmaBK>), dim3((unsigned)blocks), dim3(kGemmThreads), 0,
-                       s, g);
+    hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, false>), dim3((unsigned)blocks), dim3(kGemmThreads), 0, s, g,
+                       (char*)nullptr);
     return hipGetLastError();
 }
 
@@ -792,6 +898,11 @@ __global__ __launch_bounds__(256) void ffn_f32_down_kernel(const float* __restri
 
 }  // namespace
 
+size_t ffn_workspace_bytes() {
+    const int P = stream_k_workgroups();
+    return P > 0 ? (size_t)2 * P * kSkPartBytes : 0;
+}
+
 // Workgroup tile of the bf16 grouped GEMMs. 256-row tiles (128x128 per wave)
 // halve the LDS traffic per MFMA but pad each group to a multiple of 256
 // rows, so they are used when groups average well above that.
@@ -834,7 +945,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (up) {
         GemmParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up,
                       (uint16_t*)a.h, a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
-        hipError_t e = tile == kTileDma   ? launch_gemm_dma<true>(g1, s)
+        hipError_t e = tile == kTileDma   ? launch_gemm_dma<true>(g1, a.ws, a.ws_bytes, s)
                        : tile == kTile256 ? launch_gemm<true, 256, 128, 64, kFdb256>(g1, s)
                                           : launch_gemm<true, 128, 128, 64, true>(g1, s);
         if (e != hipSuccess) return e;
@@ -842,7 +953,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (down) {
         GemmParams g2{(const uint16_t*)a.h, (const uint16_t*)a.w_down, nullptr, (uint16_t*)a.y,
                       a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff};
-        return tile == kTileDma   ? launch_gemm_dma<false>(g2, s)
+        return tile == kTileDma   ? launch_gemm_dma<false>(g2, a.ws, a.ws_bytes, s)
                : tile == kTile256 ? launch_gemm<false, 256, 256, 64, kFdb256>(g2, s)
                                   : launch_gemm<false, 128, 256, 64, true>(g2, s);
     }

@@ -78,8 +78,13 @@ def test_workspace_bytes():
     d = good_desc(T=1000, E=16, G=16)
     n = B.workspace_bytes(d, B.STAGE_DISPATCH)
     assert n == 256 + 4 * 16 * 8  # header + ceil(1000/256) tiles x G status words
-    for st in (B.STAGE_ROUTE, B.STAGE_FFN, B.STAGE_COMBINE):
+    for st in (B.STAGE_ROUTE, B.STAGE_COMBINE):
         assert B.workspace_bytes(d, st) == 0
+    # FFN: two fp32 256x256 accumulator tiles per CU of the current device (none
+    # without a device, and none for fp32 layers)
+    n = B.workspace_bytes(d, B.STAGE_FFN)
+    assert n % (2 * 256 * 256 * 4) == 0
+    assert B.workspace_bytes(d.replace(dtype=0), B.STAGE_FFN) == 0
     assert B.workspace_bytes(good_desc(E=0), B.STAGE_DISPATCH) == 0
 
 
@@ -102,14 +107,18 @@ def test_entry_points_reject_before_launch(lib):
                                      ctypes.c_void_p(0x10010), need, z) == ALIGN
     assert lib.brownout_moe_dispatch(bd, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == NULL
     # ffn (and its halves)
-    assert lib.brownout_moe_ffn(9, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == UNSUP
-    assert lib.brownout_moe_ffn(1, 0, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
-    assert lib.brownout_moe_ffn(1, 257, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
-    assert lib.brownout_moe_ffn(1, 4, 128, 250, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
-    assert lib.brownout_moe_ffn(1, 4, 128, 256, 512, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == NULL
-    assert lib.brownout_moe_ffn(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
-    assert lib.brownout_moe_ffn_gate_up(1, 4, 128, 256, 512, FAKE, z, FAKE, FAKE, FAKE, z) == NULL
-    assert lib.brownout_moe_ffn_down(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, MISALIGNED, z) == ALIGN
+    ffn = lib.brownout_moe_ffn
+    assert ffn(9, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == UNSUP
+    assert ffn(1, 0, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    assert ffn(1, 257, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    assert ffn(1, 4, 128, 250, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    assert ffn(1, 4, 128, 256, 512, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == NULL
+    assert ffn(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z, 0, z) == ALIGN
+    # the stream-K workspace must be 256-byte aligned
+    assert ffn(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x10010), 1 << 30,
+               z) == ALIGN
+    assert lib.brownout_moe_ffn_gate_up(1, 4, 128, 256, 512, FAKE, z, FAKE, FAKE, FAKE, z, 0, z) == NULL
+    assert lib.brownout_moe_ffn_down(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, MISALIGNED, z, 0, z) == ALIGN
     # combine
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, z, z, z) == NULL
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
@@ -122,7 +131,7 @@ def test_zero_tokens_needs_no_pointers(lib):
     assert lib.brownout_moe_route(bd, z, z, z, z, z, z, z, z, z, z, z) == OK
     assert lib.brownout_moe_dispatch(bd, z, z, z, z, z, z, z, z, 0, z) == OK
     assert lib.brownout_moe_combine(bd, z, z, z, z, z, z) == OK
-    assert lib.brownout_moe_ffn(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z) == OK
+    assert lib.brownout_moe_ffn(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z, 0, z) == OK
 
 
 def test_binding_refuses_host_tensors():

@@ -223,8 +223,20 @@ LARGE_TILE_FFN = [
 ]
 
 
+def ffn_workspace():
+    """The stream-K FFN workspace of the current device."""
+    n = B.workspace_bytes(B.make_desc(1, 64, 1, 1, 1, 64, dtype="bf16"), B.STAGE_FFN)
+    assert n > 0
+    return torch.empty(n, dtype=torch.uint8, device="cuda")
+
+
+@pytest.mark.parametrize("stream_k", [False, True], ids=["tile-per-wg", "stream-k"])
 @pytest.mark.parametrize("sizes,cap,d,f", LARGE_TILE_FFN, ids=[f"seg{len(c[0])}-d{c[2]}-f{c[3]}" for c in LARGE_TILE_FFN])
-def test_ffn_large_tile_paths(sizes, cap, d, f):
+def test_ffn_large_tile_paths(sizes, cap, d, f, stream_k, monkeypatch):
+    """256-row tiles; with the stream-K workspace (and the split threshold at
+    zero) these small problems have fewer tiles than CUs, so every tile's K
+    loop is cut into several pieces that meet in the workspace."""
+    monkeypatch.setenv("BMOE_FFN_SPLIT_MIN_IDLE", "0")
     r = np.random.default_rng(len(sizes) * 1000 + d)
     nseg = len(sizes)
     offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
@@ -236,12 +248,65 @@ def test_ffn_large_tile_paths(sizes, cap, d, f):
     ref_y, ref_h = oracle.ffn(offsets, W.bf16_bits_to_f32(a)[:max(N, 1)],
                               *(W.bf16_bits_to_f32(t) for t in (wg, wu, wd)), want_h=True)
     y = torch.full((cap, d), -5.0, dtype=torch.bfloat16, device="cuda")
+    ws = ffn_workspace() if stream_k else None
+    if ws is not None:
+        ws.fill_(0xFF)  # stale contents must not matter
     yg, hg = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
-                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"), y=y)
+                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"), y=y, workspace=ws)
     torch.cuda.synchronize()
     assert_close_rows(host_f32(hg[:N]), ref_h, "bf16", "h")
     assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
     assert bool((yg[N:] == -5.0).all()), "rows past offsets[n_seg] must not be written"
+
+
+def test_ffn_stream_k_full_rounds_and_reuse(monkeypatch):
+    """More tiles than two rounds of workgroups (full rounds, then the split
+    remainder); the workspace is reused by a second, smaller call; results
+    match the tile-per-workgroup path within bf16 rounding and are
+    deterministic."""
+    r = np.random.default_rng(77)
+    d, f = 512, 1024
+    # gate/up: 77 M-tiles x 8 N-tiles = 616 tiles (one whole round on 256 CUs,
+    # then the split); down: 154 tiles (split only)
+    sizes = (6000, 5000, 8000, 1)
+    cap = 20480
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N = int(offsets[-1])
+    nseg = len(sizes)
+    a = dev_tensor(W.f32_to_bf16_bits(r.standard_normal((cap, d)).astype(np.float32)), "bf16")
+    wg = dev_tensor(W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32)), "bf16")
+    wu = dev_tensor(W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32)), "bf16")
+    wd = dev_tensor(W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / np.sqrt(f)).astype(np.float32)), "bf16")
+    offs = torch.from_numpy(offsets).cuda()
+    ws = ffn_workspace()
+    monkeypatch.setenv("BMOE_FFN_SPLIT_MIN_IDLE", "0")  # split whenever whole tiles leave CUs idle
+    y0, h0 = B.ffn(offs, a, wg, wu, wd)
+    y1, h1 = B.ffn(offs, a, wg, wu, wd, workspace=ws)
+    y2, h2 = B.ffn(offs, a, wg, wu, wd, workspace=ws)
+    torch.cuda.synchronize()
+    # rows past offsets[n_seg] are never written (the buffers are uninitialised there)
+    assert torch.equal(y1[:N].view(torch.int16), y2[:N].view(torch.int16))
+    assert torch.equal(h1[:N].view(torch.int16), h2[:N].view(torch.int16))
+    assert_close_rows(host_f32(h1[:N]), host_f32(h0[:N]), "bf16", "h")
+    assert_close_rows(host_f32(y1[:N]), host_f32(y0[:N]), "bf16", "y")
+    # spot rows against the oracle (first/last row of every segment)
+    rows = sorted({int(o) for o in offsets[:-1]} | {int(o) - 1 for o in offsets[1:] if o > 0})
+    rows = [q for q in rows if q < N]
+    wg32, wu32, wd32 = host_f32(wg), host_f32(wu), host_f32(wd)
+    one = np.array([0, 1], np.int32)
+    for q in rows:
+        sg = int(np.searchsorted(offsets, q, side="right") - 1)
+        ref_y, ref_h = oracle.ffn(one, host_f32(a[q:q + 1]), wg32[sg:sg + 1], wu32[sg:sg + 1], wd32[sg:sg + 1],
+                                  want_h=True)
+        assert_close_rows(host_f32(h1[q:q + 1]), ref_h, "bf16", f"h row {q} vs oracle")
+        assert_close_rows(host_f32(y1[q:q + 1]), ref_y, "bf16", f"y row {q} vs oracle")
+    # a smaller problem through the same (now stale) workspace
+    small = np.array([0, 700, 1500], np.int32)
+    ys, hs = B.ffn(torch.from_numpy(small).cuda(), a, wg[:2].contiguous(), wu[:2].contiguous(), wd[:2].contiguous(),
+                   workspace=ws)
+    ys0, _ = B.ffn(torch.from_numpy(small).cuda(), a, wg[:2].contiguous(), wu[:2].contiguous(), wd[:2].contiguous())
+    torch.cuda.synchronize()
+    assert_close_rows(host_f32(ys[:1500]), host_f32(ys0[:1500]), "bf16", "y small")
 
 
 # ---------------------------------------------------------------------------
