@@ -32,6 +32,35 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 VALU_F32_PEAK_TFLOPS = 157.3
 
+# HBM bytes of one launch of the gate/up GEMM kernel, from rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE runs of this bench (KiB per dispatch), scaled by
+# what the same counters read for a plain 1 GiB device copy (bench.py
+# --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
+# all of them). Valid only for the kernel sources they were taken with.
+TRAFFIC_RECORDS = {
+    "mixtral": {"src_sha1": "de9c2ffe46d9b8b6f1cca02f13b4021d7ba5b7ac",
+                "fetch_kib": 1702291.4, "write_kib": 312072.0, "fetch_scale": 2.0, "write_scale": 1.0,
+                "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
+}
+TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
+
+
+def recorded_traffic(config: str):
+    """Scaled HBM bytes per launch of the dominant kernel, or None when no
+    record exists or the kernel sources changed since it was taken."""
+    import hashlib
+    rec = TRAFFIC_RECORDS.get(config)
+    if rec is None:
+        return None
+    h = hashlib.sha1()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != rec["src_sha1"]:
+        return None
+    return int(rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"])
+
+
 WORKLOAD_TEXT = {
     "mixtral": "Mixtral-8x7B-shaped grouped MoE layer: T=4096 tokens, d=4096, E=8 experts, top-2, "
                "G=4 united experts (2 experts each, seeded map), SwiGLU d_ff=14336, bf16, "
@@ -54,7 +83,30 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="instead of the layer: time a device-to-device copy of this many MiB (the plain "
+                         "copy kernel that HBM byte counters are calibrated against)")
     return ap.parse_args()
+
+
+def copy_probe(mib: int, reps: int = 10):
+    """A plain device copy of a known size: reads and writes mib MiB per launch."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_probe_mib": mib, "bytes_read": n, "bytes_written": n, "launches": reps + 1,
+                      "ms_per_copy": round(ms, 4), "GB_s_read_plus_write": round(2 * n / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
 
 
 def main():
@@ -67,6 +119,11 @@ def main():
     import torch
     from paper_2607_04164_amd import binding as B
     from paper_2607_04164_amd import workload as W
+
+    if args.copy_probe_mib > 0:
+        torch.cuda.set_device(0)
+        copy_probe(args.copy_probe_mib)
+        return
 
     cfg = W.CONFIGS[args.config]
     print(f"[bench] generating {cfg.name} seed {args.seed}", file=sys.stderr, flush=True)
@@ -152,11 +209,12 @@ def main():
     dms = per_stage_ms[dom]
     dpeak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
     dach = damount / (dms * 1e-3) / 1e12
-    roofline = {"kernel": "grouped_gemm_kernel<gate_up> (brownout_moe_ffn_gate_up)",
+    traffic = recorded_traffic(args.config)
+    roofline = {"kernel": "grouped_gemm_dma_kernel<gated> (brownout_moe_ffn_gate_up)",
                 "bound": "mfma" if cfg.dtype == "bf16" else "alu",
                 "achieved": round(dach, 1), "peak": dpeak, "unit": "TFLOP/s",
-                "frac": round(dach / dpeak, 4), "traffic": None,
-                "per_launch": f"4*N*d*d_ff flop, N={N} rows"}
+                "frac": round(dach / dpeak, 4), "traffic": traffic,
+                "per_launch": f"4*N*d*d_ff flop, N={N} rows; traffic: HBM bytes per launch (scaled pmc)"}
 
     result = {
         "metric": "grouped-MoE layer tokens/sec on 1 MI355X; FFN MFMA util %; route/permute HBM GB/s",
