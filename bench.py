@@ -83,6 +83,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--compare-ungrouped", action="store_true",
+                    help="also time the same layer with no grouping (G = E, every expert its own group: "
+                         "zero brownout) and report the speedup of grouping")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the layer: time a device-to-device copy of this many MiB (the plain "
                          "copy kernel that HBM byte counters are calibrated against)")
@@ -109,28 +112,16 @@ def copy_probe(mib: int, reps: int = 10):
           flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs the layer on one GPU only; --gpus {args.gpus} is not supported "
-              f"(the multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
-        sys.exit(2)
-
+def time_layer(cfg, args, dev):
+    """Builds the seeded layer on the device and times args.steps full forwards
+    after args.warmup untimed ones. Returns the host layer, wall ms per step,
+    per-stage event ms, the row count N, the group row counts and the stages."""
     import torch
     from paper_2607_04164_amd import binding as B
     from paper_2607_04164_amd import workload as W
 
-    if args.copy_probe_mib > 0:
-        torch.cuda.set_device(0)
-        copy_probe(args.copy_probe_mib)
-        return
-
-    cfg = W.CONFIGS[args.config]
-    print(f"[bench] generating {cfg.name} seed {args.seed}", file=sys.stderr, flush=True)
+    print(f"[bench] generating {cfg.name} (G={cfg.G}) seed {args.seed}", file=sys.stderr, flush=True)
     L = W.make_layer(cfg, args.seed)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    B.load_library()
 
     def to_dev(a):
         if cfg.dtype == "bf16":
@@ -179,6 +170,32 @@ def main():
     ms_step = wall * 1e3 / args.steps
     per_stage_ms = {s: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
                     for i, s in enumerate(stages)}
+    del layer, w, x
+    torch.cuda.empty_cache()
+    return L, ms_step, per_stage_ms, N, counts, stages
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs the layer on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_04164_amd import binding as B
+    from paper_2607_04164_amd import workload as W
+
+    if args.copy_probe_mib > 0:
+        torch.cuda.set_device(0)
+        copy_probe(args.copy_probe_mib)
+        return
+
+    cfg = W.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B.load_library()
+    L, ms_step, per_stage_ms, N, counts, stages = time_layer(cfg, args, dev)
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
@@ -237,6 +254,14 @@ def main():
         "stages": stage_out,
         "cpu_baseline": None,
     }
+
+    if args.compare_ungrouped and cfg.G != cfg.E:
+        ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E)
+        _, ms_u, stages_u, N_u, _, _ = time_layer(ucfg, args, dev)
+        result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
+                               "ms_per_step": round(ms_u, 4),
+                               "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},
+                               "grouped_speedup": round(ms_u / ms_step, 3)}
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)

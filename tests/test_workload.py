@@ -56,3 +56,18 @@ def test_value_distributions():
 def test_sequential_map_is_index_order():
     assert W.sequential_map(6, 2).tolist() == [0, 0, 1, 1, 2, 2]
     assert W.sequential_map(60, 4).max() == 14
+
+
+def test_routed_load_is_as_skewed_as_the_paper_reports():
+    """Sec. 2.3 (challenge C1): on the paper's 60-expert model the ten most
+    used experts take more than 40 % of the routed tokens and the twenty least
+    used fewer than 10 %. The synthetic skew of the 60-expert workload must be
+    at least that strong (top-k picks on float64 logits of 2048 of its tokens)."""
+    cfg = W.CONFIGS["fine"]
+    L = W.make_layer(cfg, 0, with_weights=False)
+    n = 2048
+    z = L.f32("x")[:n].astype(np.float64) @ L.f32("w_router").astype(np.float64).T + L.bias
+    picks = np.argsort(-z, axis=1, kind="stable")[:, :cfg.top_k]
+    load = np.sort(np.bincount(picks.ravel(), minlength=cfg.E))[::-1] / picks.size
+    assert load[:10].sum() > 0.40, load[:10].sum()
+    assert load[-20:].sum() < 0.10, load[-20:].sum()
