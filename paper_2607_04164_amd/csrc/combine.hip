@@ -3,7 +3,10 @@
 // always-on shared-expert output when there is one.
 // One wave per token; each lane owns 16-byte column chunks; the slot rows are
 // gathered with 128-bit loads, accumulated in fp32 in slot order, and the row
-// is written once with 128-bit stores.
+// is written once with 128-bit streaming stores. When the expert-output buffer
+// (its row capacity times the row size) is larger than the last-level cache
+// (256 MiB) its rows are read with streaming loads too; smaller ones are often
+// still cached from the down projection.
 #include "bmoe_common.h"
 
 namespace bmoe {
@@ -46,7 +49,7 @@ struct Vec<float> {  // 4 floats per chunk
     }
 };
 
-template <typename E, int U>
+template <typename E, int U, bool STREAM_IN>
 __global__ __launch_bounds__(256) void combine_kernel(const int32_t* __restrict__ slot_row,
                                                       const float* __restrict__ slot_gate,
                                                       const uint4* __restrict__ y,
@@ -79,7 +82,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const int32_t* __restrict_
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int c = c0 + 64 * u;
-                v[u] = c < nch ? src[c] : make_uint4(0, 0, 0, 0);
+                v[u] = c < nch ? (STREAM_IN ? load_stream(src + c) : src[c]) : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -106,9 +109,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const int32_t* __restrict_
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + 64 * u;
-            if (c < nch) dst[c] = Vec<E>::store(acc[u]);
+            if (c < nch) store_stream(dst + c, Vec<E>::store(acc[u]));
         }
     }
+}
+
+template <typename E, bool STREAM_IN>
+void launch_combine_t(const CombineArgs& a, int nch, hipStream_t s) {
+    hipLaunchKernelGGL((combine_kernel<E, 4, STREAM_IN>), dim3(ceil_div(a.T, 4)), dim3(256), 0, s,
+                       a.slot_row, a.slot_gate, (const uint4*)a.y, (const uint4*)a.y_shared,
+                       (uint4*)a.out, a.T, a.k, nch, a.rows_cap);
 }
 
 }  // namespace
@@ -116,15 +126,15 @@ __global__ __launch_bounds__(256) void combine_kernel(const int32_t* __restrict_
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
     if (a.T == 0) return hipSuccess;
     const int nch = a.d * a.elem_bytes / 16;
-    dim3 grid(ceil_div(a.T, 4));
-    if (a.elem_bytes == 2)
-        hipLaunchKernelGGL((combine_kernel<uint16_t, 4>), grid, dim3(256), 0, s, a.slot_row, a.slot_gate,
-                           (const uint4*)a.y, (const uint4*)a.y_shared, (uint4*)a.out, a.T, a.k, nch,
-                           a.rows_cap);
-    else
-        hipLaunchKernelGGL((combine_kernel<float, 4>), grid, dim3(256), 0, s, a.slot_row, a.slot_gate,
-                           (const uint4*)a.y, (const uint4*)a.y_shared, (uint4*)a.out, a.T, a.k, nch,
-                           a.rows_cap);
+    const int64_t rows = a.rows_cap < (int64_t)a.T * a.k ? a.rows_cap : (int64_t)a.T * a.k;
+    const bool stream_in = rows * a.d * a.elem_bytes >= ((int64_t)256 << 20);
+    if (a.elem_bytes == 2) {
+        if (stream_in) launch_combine_t<uint16_t, true>(a, nch, s);
+        else launch_combine_t<uint16_t, false>(a, nch, s);
+    } else {
+        if (stream_in) launch_combine_t<float, true>(a, nch, s);
+        else launch_combine_t<float, false>(a, nch, s);
+    }
     return hipGetLastError();
 }
 

@@ -8,7 +8,9 @@
 //     slot's stable rank inside the tile;
 //   - single-pass decoupled look-back: the tile publishes its counts, walks
 //     back over earlier tiles' published counts / inclusive prefixes until it
-//     meets a prefix, then publishes its own inclusive prefix;
+//     meets a prefix (a segment of a wave's lanes per group, reading as many
+//     predecessors per step as it has lanes), then
+//     publishes its own inclusive prefix;
 //   - slot_row receives the row relative to the group start; the last tile
 //     writes the group counts and their exclusive prefix (offsets).
 // Kernel 2 (permute), one wave per token: adds offsets[group] to the relative
@@ -80,36 +82,64 @@ __global__ __launch_bounds__(kTile) void hist_scan_kernel(const int32_t* __restr
 #pragma unroll
         for (int w = 0; w < kTile / 64; ++w) c += __popcll(masks[tid][w]);
         s_cnt[tid] = c;
-        uint64_t* my = status + (size_t)tile * G + tid;
-        int excl = 0;
-        if (tile == 0) {
-            __hip_atomic_store(my, pack_status(kFlagPrefix, (uint32_t)c), __ATOMIC_RELEASE,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            __hip_atomic_store(my, pack_status(kFlagAgg, (uint32_t)c), __ATOMIC_RELEASE,
-                               __HIP_MEMORY_SCOPE_AGENT);
-            // look back; every earlier tile took its ticket before this one and
-            // publishes without waiting on anything, so the walk terminates
-            int j = tile - 1;
-            int polls = 0;
-            while (true) {
-                uint64_t sv = __hip_atomic_load(status + (size_t)j * G + tid, __ATOMIC_ACQUIRE,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-                uint32_t flag = (uint32_t)(sv >> 32);
-                if (flag == 0u) {
-                    if (++polls > kMaxPolls) break;
-                    __builtin_amdgcn_s_sleep(1);
-                    continue;
-                }
-                polls = 0;
-                excl += (int)(uint32_t)sv;
-                if (flag == kFlagPrefix) break;
-                --j;
+        __hip_atomic_store(status + (size_t)tile * G + tid,
+                           pack_status(tile == 0 ? kFlagPrefix : kFlagAgg, (uint32_t)c),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+
+    // Look-back. Each wave takes gpw groups (a power of two, 4 * gpw >= G) and
+    // gives each a segment of lpg = 64 / gpw lanes; lane i of a segment reads
+    // the status of tile j0 - i, so one round trip covers lpg predecessors of
+    // every group of the wave. Every earlier tile took its ticket before this
+    // one and publishes its counts without waiting on anything, so each window
+    // fills and the walk terminates. A status word holds both its flag and its
+    // count and nothing else is published through it, so relaxed device-scope
+    // atomics suffice (acquire/release would add an L2 invalidate or write-back
+    // to every poll and publish).
+    {
+        const int wave = tid >> 6, lane = tid & 63;
+        int gpw = 1;
+        while (gpw * (kTile / 64) < G) gpw <<= 1;
+        const int lpg = 64 / gpw;
+        const int sl = lane & (lpg - 1), sb = lane - sl;
+        const uint64_t segmask = lpg == 64 ? ~0ull : ((1ull << lpg) - 1ull);
+        const int g = wave * gpw + lane / lpg;
+        const bool gv = g < G;
+        const int c = gv ? s_cnt[g] : 0;
+        int excl = 0, j0 = tile - 1, polls = 0;
+        bool done = !gv || j0 < 0;
+        while (__ballot(!done) != 0ull) {
+            const int j = j0 - sl;
+            uint64_t sv = pack_status(kFlagPrefix, 0u);
+            if (!done && j >= 0)
+                sv = __hip_atomic_load(status + (size_t)j * G + g, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            const uint32_t flag = (uint32_t)(sv >> 32);
+            const uint64_t pm = (__ballot(flag == kFlagPrefix) >> sb) & segmask;
+            const uint64_t zm = (__ballot(flag == 0u) >> sb) & segmask;
+            const int np = pm ? __ffsll((unsigned long long)pm) - 1 : lpg;  // nearest prefix
+            const uint64_t need = np >= lpg ? segmask : ((2ull << np) - 1ull);
+            const bool wait = !done && (zm & need) != 0ull;
+            int v = (!done && !wait && sl <= np) ? (int)(uint32_t)sv : 0;
+            for (int m = lpg >> 1; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+            if (!done && !wait) {
+                excl += v;
+                if (np < lpg) done = true;
+                else j0 -= lpg;
             }
-            __hip_atomic_store(my, pack_status(kFlagPrefix, (uint32_t)(excl + c)), __ATOMIC_RELEASE,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(wait) != 0ull) {
+                if (++polls > kMaxPolls) break;  // workspace was not zeroed
+                __builtin_amdgcn_s_sleep(1);
+            }
         }
-        s_excl[tid] = excl;
+        if (gv && sl == 0) {
+            if (tile > 0)
+                __hip_atomic_store(status + (size_t)tile * G + g,
+                                   pack_status(kFlagPrefix, (uint32_t)(excl + c)), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            s_excl[g] = excl;
+        }
     }
     __syncthreads();
 
@@ -192,7 +222,7 @@ __global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict_
 #pragma unroll
                 for (int u = 0; u < VEC; ++u) {
                     const int c = c0 + 64 * u;
-                    if (c < nch) dst[c] = v[u];
+                    if (c < nch) store_stream(dst + c, v[u]);
                 }
             }
         }

@@ -143,9 +143,15 @@ def test_dispatch_exact(name, seed):
 
 
 def test_dispatch_many_tiles_and_reuse():
-    """Several calls in a row on one workspace, T spanning many 256-token tiles."""
+    """Several calls in a row on one workspace, T spanning many 256-token tiles.
+
+    The group counts cover every width of the look-back's lane segments (64
+    lanes per group for G <= 4 down to one lane for G = 256), and the longer
+    runs need more than one look-back window per group.
+    """
     r = np.random.default_rng(3)
-    for T, k, G in ((5000, 6, 16), (777, 2, 4), (256, 4, 15), (1, 1, 1), (4097, 8, 64)):
+    for T, k, G in ((5000, 6, 16), (777, 2, 4), (256, 4, 15), (1, 1, 1), (4097, 8, 64),
+                    (40000, 2, 4), (30000, 3, 3), (17000, 5, 5), (9000, 4, 33), (3000, 8, 256)):
         sg = r.integers(-1, G, size=(T, k)).astype(np.int32)
         for t in range(T):  # at most one valid slot per group per token, as route guarantees
             seen = set()
@@ -157,7 +163,7 @@ def test_dispatch_many_tiles_and_reuse():
         ref = oracle.dispatch(sg, G)
         desc = B.make_desc(T, 64, max(G, k), k, G, 64)
         x = torch.randn(T, 64, device="cuda").to(torch.bfloat16)
-        ws = B.new_dispatch_workspace(B.make_desc(5000, 64, 64, 8, 64, 64), "cuda")
+        ws = B.new_dispatch_workspace(B.make_desc(40000, 64, 256, 8, 256, 64), "cuda")
         for _ in range(2):
             got = B.dispatch(desc, torch.from_numpy(sg).cuda(), x, ws)
             torch.cuda.synchronize()
