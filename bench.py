@@ -170,9 +170,23 @@ def time_layer(cfg, args, dev):
     ms_step = wall * 1e3 / args.steps
     per_stage_ms = {s: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
                     for i, s in enumerate(stages)}
+    # each stage alone, launched back to back (the in-step events above also
+    # hold the gaps between kernels, which dominate the short stages)
+    iso_ms = {}
+    for s in stages:
+        reps = 3 if s.startswith("ffn") or s == "shared_ffn" else 20
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        calls[s]()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            calls[s]()
+        e1.record()
+        torch.cuda.synchronize()
+        iso_ms[s] = e0.elapsed_time(e1) / reps
     del layer, w, x
     torch.cuda.empty_cache()
-    return L, ms_step, per_stage_ms, N, counts, stages
+    return L, ms_step, per_stage_ms, iso_ms, N, counts, stages
 
 
 def main():
@@ -195,7 +209,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B.load_library()
-    L, ms_step, per_stage_ms, N, counts, stages = time_layer(cfg, args, dev)
+    L, ms_step, per_stage_ms, iso_ms, N, counts, stages = time_layer(cfg, args, dev)
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
@@ -207,19 +221,22 @@ def main():
         "shared_ffn": ("mfma", 6.0 * T * d * cfg.d_ff_shared),
         "combine": ("hbm", T * k * 8 + N * d * s + T * d * s * (2 if cfg.n_shared else 1)),
     }
+    # per stage: "us" and the rates from the stage launched alone back to back,
+    # "in_step_us" from the events around it inside the timed steps
     stage_out = {}
     for st_name in stages:
         kind, amount = work[st_name]
-        ms = per_stage_ms[st_name]
+        ms = iso_ms[st_name]
         if kind == "hbm":
             rate = amount / (ms * 1e-3) / 1e9
-            stage_out[st_name] = {"us": round(ms * 1e3, 2), "bytes": int(amount), "GB_s": round(rate, 1),
+            stage_out[st_name] = {"us": round(ms * 1e3, 2), "in_step_us": round(per_stage_ms[st_name] * 1e3, 2),
+                                  "bytes": int(amount), "GB_s": round(rate, 1),
                                   "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
         else:
             peak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
             rate = amount / (ms * 1e-3) / 1e12
-            stage_out[st_name] = {"us": round(ms * 1e3, 2), "flop": amount, "TFLOP_s": round(rate, 1),
-                                  "frac_of_peak": round(rate / peak, 4)}
+            stage_out[st_name] = {"us": round(ms * 1e3, 2), "in_step_us": round(per_stage_ms[st_name] * 1e3, 2),
+                                  "flop": amount, "TFLOP_s": round(rate, 1), "frac_of_peak": round(rate / peak, 4)}
 
     dom = "ffn_gate_up"
     dkind, damount = work[dom]
@@ -257,7 +274,7 @@ def main():
 
     if args.compare_ungrouped and cfg.G != cfg.E:
         ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E)
-        _, ms_u, stages_u, N_u, _, _ = time_layer(ucfg, args, dev)
+        _, ms_u, stages_u, _, N_u, _, _ = time_layer(ucfg, args, dev)
         result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
                                "ms_per_step": round(ms_u, 4),
                                "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},

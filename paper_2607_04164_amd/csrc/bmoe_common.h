@@ -41,17 +41,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi) {
 
 // silu(g) * u = g / (1 + e^-g) * u with the hardware exp2 and reciprocal
 // (relative error ~1e-7, far below the bf16 rounding that follows)
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-// Streaming 128-bit store and load (nontemporal hint): for rows that one
-// kernel writes or reads exactly once, so they do not displace reused lines.
-__device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
-    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), (u32x4*)p);
-}
-__device__ __forceinline__ uint4 load_stream(const uint4* p) {
-    return __builtin_bit_cast(uint4, __builtin_nontemporal_load((const u32x4*)p));
-}
-
 __device__ __forceinline__ float silu_mul(float g, float u) {
     return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)) * u;
 }

@@ -8,6 +8,7 @@
 // (256 MiB) its rows are read with streaming loads too; smaller ones are often
 // still cached from the down projection.
 #include "bmoe_common.h"
+#include "stream_io.h"
 
 namespace bmoe {
 namespace {

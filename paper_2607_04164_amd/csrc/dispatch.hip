@@ -17,6 +17,7 @@
 // row, writes perm_token, and copies x[t] into each of its rows with 128-bit
 // loads and stores. Workgroup 0 clears the look-back state for the next call.
 #include "bmoe_common.h"
+#include "stream_io.h"
 
 namespace bmoe {
 namespace {

@@ -4,7 +4,7 @@
 // One workgroup (4 waves) owns BT = 16*TB tokens:
 //   1. logits tile [BT, E] into LDS:
 //        bf16: x rows and W_router rows are copied straight into LDS
-//              (global_load_lds, swizzled rows) in super-chunks of KS*64
+//              (global_load_lds, swizzled rows) in super-chunks of KS*KW*64
 //              columns through a ring of slots shared by the 4 waves;
 //              16x16x32 bf16 MFMA, fp32 accumulate; with KS > 1 the waves
 //              split the d axis and their partial tiles are summed in LDS
@@ -12,17 +12,22 @@
 //        f32:  one (token, expert) dot product per thread;
 //        logits_in: copied.
 //   2. per token, a group of S lanes (S <= 16, chosen so that a wave's tokens
-//      fill it) holds the E logits; k+1 rounds of group arg-max (DPP within
-//      rows of 16 lanes) give the picks in order (ties: lower expert index).
-//      If two adjacent values among the top k+1 are closer than
+//      fill it) holds the E logits, V <= 16 per lane; k+1 rounds of a
+//      branch-free local scan and a group arg-max (DPP within rows of 16
+//      lanes) give the picks in order (ties: lower expert index); the arg-max
+//      key packs the expert id with its united expert, so a round touches no
+//      memory. If two adjacent values among the top k+1 are closer than
 //      BMOE_ROUTE_RECHECK_GAP the token is queued for step 3. Otherwise
-//      softmax, optional renormalisation, the map and the per-group merge
-//      are done from the token's pick list and written out.
-//   3. a queued token is decided again in float64 by the wave that queued it:
-//      every expert whose fp32 logit is within the gap of the k-th value is
-//      recomputed from exact float64 products, and the top-k is taken among
-//      those by ranking them.
+//      softmax, optional renormalisation and the per-group merge are done
+//      from the token's pick list and written out.
+//   3. queued tokens are decided again in float64 by teams of waves (a lone
+//      token gets all four, each summing a quarter of the row): every expert
+//      whose fp32 logit is within the gap of the k-th value is recomputed
+//      from exact float64 products, and the top-k is taken among those by
+//      ranking them.
 #include "bmoe_common.h"
+
+#include <atomic>
 
 namespace bmoe {
 namespace {
@@ -39,9 +44,10 @@ struct RouteSmem {
     __host__ __device__ size_t total() const { return zs_bytes + flag_bytes + cand_bytes + dummy_bytes + ring_bytes; }
 };
 
-template <int TB, int NBLK>
+template <int TB, int NBLK, int KW>
 struct RouteCfg {
-    static constexpr int BT = 16 * TB, KS = 4 / TB, KC = 64 * KS, EP = 16 * NBLK;
+    // KW: 64-column units each wave multiplies per super-chunk
+    static constexpr int BT = 16 * TB, KS = 4 / TB, KC = 64 * KS * KW, EP = 16 * NBLK;
     static constexpr int CPR = KC / 8;                // 16-byte chunks per LDS row
     static constexpr int RPD = 64 / CPR;              // rows per DMA instruction (1 KB)
     static constexpr int SWZ = CPR >= 16 ? 15 : 7;    // swizzle mask of the chunk index
@@ -58,12 +64,13 @@ struct RouteCfg {
     static constexpr int PART = (KS - 1) * BT * EP * 4;
     static constexpr int TOTAL = ZS + FLAG + CAND + DUMMY + NSLOT * SLOT;
     static_assert(NSLOT >= 2, "at least two slots");
+    static_assert(CPR <= 64, "a copy instruction covers whole rows");
     static_assert(PART <= NSLOT * SLOT, "partials alias the ring");
     static_assert(TOTAL <= 160 * 1024, "LDS of one workgroup");
     static_assert(DPW * (NSLOT - 2) <= 63, "vmcnt range");
 };
 
-template <int MODE, int TB, int NBLK>
+template <int MODE, int TB, int NBLK, int KW>
 __host__ __device__ inline RouteSmem route_smem(int E) {
     RouteSmem s;
     const int bt = 16 * TB;
@@ -73,7 +80,7 @@ __host__ __device__ inline RouteSmem route_smem(int E) {
     s.flag_bytes = 2048;
     s.cand_bytes = 4 * 2048;
     s.dummy_bytes = (MODE == MODE_BF16) ? 4 * 1024 : 0;
-    s.ring_bytes = (MODE == MODE_BF16) ? (size_t)RouteCfg<TB, NBLK>::NSLOT * RouteCfg<TB, NBLK>::SLOT : 0;
+    s.ring_bytes = (MODE == MODE_BF16) ? (size_t)RouteCfg<TB, NBLK, KW>::NSLOT * RouteCfg<TB, NBLK, KW>::SLOT : 0;
     return s;
 }
 
@@ -147,12 +154,17 @@ __device__ __forceinline__ V group_sum(V v) {
     return v;
 }
 
-// A pick in a token's pick list: expert id in the low 16 bits, united expert + 1
-// in the high bits (0: the map sends the expert nowhere, so the slot calls none).
+// A pick in a token's pick list: expert id in the high bits, united expert + 1
+// in the low 16 bits (0: the map sends the expert nowhere, so the slot calls
+// none). Keys of distinct experts order like their expert ids, so the packed
+// value serves as the tie-break index of an arg-max.
+constexpr int kNoPick = 0x7fff0000;  // out-of-range expert, no united expert
 __device__ __forceinline__ int pack_pick(int e, const int* e2g_s, int E) {
     const int g = (unsigned)e < (unsigned)E ? e2g_s[e] : -1;  // NaN logits pick nothing
-    return (e & 0xffff) | ((g + 1) << 16);
+    return ((e & 0x7fff) << 16) | (g + 1);
 }
+__device__ __forceinline__ int pick_expert(int pk) { return pk >> 16; }
+__device__ __forceinline__ int pick_group(int pk) { return (pk & 0xffff) - 1; }
 
 // Softmax weights, optional renormalisation and per-group merge of one token
 // from its pick list (pk: packed picks, pkv: their logits, largest first),
@@ -171,7 +183,7 @@ __device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, i
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int q = s + i * S;
-        gq[i] = q < k ? (pk[q] >> 16) - 1 : -3;
+        gq[i] = q < k ? pick_group(pk[q]) : -3;
         eq[i] = 0.f;
         gs[i] = 0.f;
         dup[i] = false;
@@ -179,7 +191,7 @@ __device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, i
     float tot = 0.f;
 #pragma unroll 4
     for (int j = 0; j < k; ++j) {
-        const int g = (pk[j] >> 16) - 1;
+        const int g = pick_group(pk[j]);
         const float ex = __expf((float)(pkv[j] - top));
         tot += ex;
 #pragma unroll
@@ -199,7 +211,7 @@ __device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, i
         const int q = s + i * S;
         if (q >= k) break;
         const size_t o = (size_t)t * k + q;
-        p.topk_idx[o] = pk[q] & 0xffff;
+        p.topk_idx[o] = pick_expert(pk[q]);
         p.topk_w[o] = eq[i] * inv;
         const bool valid = !dup[i] && gq[i] >= 0;
         p.slot_group[o] = valid ? gq[i] : -1;
@@ -221,63 +233,70 @@ struct SelectCtx {
     bool recheck;
 };
 
-template <int S, int TPW>
+template <int S, int V, int TPW>
 __device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCtx& c, int lane) {
     constexpr int P = kWave / S;
     const int E = p.E, k = p.k;
-    const int VPL = (E + S - 1) / S;
     const int s = lane % S, seg = lane / S;
     const int R = min(k + 1, E);
-    constexpr int kNone = 0x7fffffff;
+    // this lane holds experts s, s+S, ... below E (vpl <= V of them); the other
+    // value slots start out taken, so the rounds need no bounds test
+    const int vpl = (E - s + S - 1) / S;
+    const unsigned dead = vpl >= V ? 0u : ~0u << vpl;
+    int key[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        const int e = s + j * S;
+        key[j] = j < vpl ? pack_pick(e, c.e2g_s, E) : kNoPick;
+    }
+#pragma unroll
     for (int base = 0; base < TPW; base += P) {
         const int tw = base + seg;
         if (tw >= TPW) continue;
         const bool tok_ok = c.t0 + c.tw0 + tw < p.T;
         const int tl = tok_ok ? c.tw0 + tw : 0;
-        float v[16];
+        float v[V];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int e = s + j * S;
-            v[j] = -INFINITY;
-            if (j < VPL) v[j] = e < E ? c.zs[tl * c.zstride + e] : -INFINITY;
+        for (int j = 0; j < V; ++j) {
+            const int e = min(s + j * S, E - 1);
+            const float z = c.zs[tl * c.zstride + e];
+            v[j] = j < vpl ? z : -INFINITY;
         }
         // the picks go to the pick area (every lane of the group writes the
         // same values); registers indexed by the round would need dynamic
         // register indexing
         int* pk = c.area + tw * 32;
         float* pkv = (float*)(pk + 16);
-        unsigned taken = 0;
+        unsigned taken = dead;
         float prev = 0.f, top = 0.f, kth = 0.f;
         bool close = false;
         for (int r = 0; r < R; ++r) {
             // local arg-max in ascending expert order: strict > keeps the lower
-            // index on ties; padding lanes hold -inf and lose to any expert
+            // index on ties; the first untaken slot is taken even at -inf
             float bv = -INFINITY;
-            int be = kNone;
+            int be = kNoPick;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                if (j < VPL) {
-                    const bool t = !((taken >> j) & 1u) && (v[j] > bv || be == kNone);
-                    bv = t ? v[j] : bv;
-                    be = t ? s + j * S : be;
-                }
+            for (int j = 0; j < V; ++j) {
+                const bool t = !((taken >> j) & 1u) && (v[j] > bv || be == kNoPick);
+                bv = t ? v[j] : bv;
+                be = t ? key[j] : be;
             }
             group_argmax<S>(bv, be);
-            if (be % S == s) taken |= 1u << (be / S);
+            const int e = pick_expert(be);
+            if ((e & (S - 1)) == s) taken |= 1u << ((e / S) & 31);
             if (r < k) {
-                pk[r] = pack_pick(be, c.e2g_s, E);
+                pk[r] = be;
                 pkv[r] = bv;
             }
-            if (r == 0) top = bv;
-            if (r == k - 1) kth = bv;
-            if (r > 0 && prev - bv < kGap) close = true;
+            top = r == 0 ? bv : top;
+            kth = r == k - 1 ? bv : kth;
+            close = close || (r > 0 && prev - bv < kGap);
             prev = bv;
         }
         close = close && c.recheck;
         float se = 0.f;
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-            if (j < VPL) se += __expf(v[j] - top);
+        for (int j = 0; j < V; ++j) se += j < vpl ? __expf(v[j] - top) : 0.f;
         se = group_sum<S>(se);
         finish_token<float>(p, c.t0 + tl, s, S, pk, pkv, top, se, tok_ok && !close);
         if (tok_ok && close && s == 0) {
@@ -288,60 +307,67 @@ __device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCt
     }
 }
 
+// Values per lane: the smallest of 1, 4, 16 that holds ceil(E / S). With S
+// below 64 / TPW the group already spans all experts (V = 1); above it, S was
+// raised because E needs more than 8 values per lane (V = 16).
+template <int S, int TPW>
+__device__ __forceinline__ void select_tokens_v(const RouteArgs& p, const SelectCtx& c, int lane) {
+    constexpr int SB = kWave / TPW;
+    const int vpl = (p.E + S - 1) / S;
+    if constexpr (S < SB) {
+        select_tokens<S, 1, TPW>(p, c, lane);
+    } else if constexpr (S > SB) {
+        select_tokens<S, 16, TPW>(p, c, lane);
+    } else {
+        if (vpl <= 1) select_tokens<S, 1, TPW>(p, c, lane);
+        else if (vpl <= 4) select_tokens<S, 4, TPW>(p, c, lane);
+        else select_tokens<S, 16, TPW>(p, c, lane);
+    }
+}
+
 // Exact-product float64 dot products of one token row with up to 8 router rows
-// (ids[i] < 0: unused; the used ids come first). bf16 and fp32 products are
-// exact in float64. Lane l takes the 16-byte chunks l, l+64, ... of the rows
-// (coalesced); a block of 4 chunks per lane is loaded together with the same
-// chunks of four router rows, so a token with up to 4 candidates costs one
-// memory latency per 2048 bf16 columns; each lane sums its chunks in order,
-// then the wave reduces.
+// over the 16-byte chunks [cb, ce) of the rows (ids[i] < 0: unused; the used
+// ids come first). bf16 and fp32 products are exact in float64. Lane l takes
+// the chunks cb+l, cb+l+64, ... (coalesced); a block of U chunks per lane is
+// loaded together with the same chunks of every used router row, so a range of
+// up to U*64 chunks costs one memory latency; each lane sums its chunks in
+// order, then the wave reduces.
 template <int MODE>
-__device__ __forceinline__ void dot_f64_batch(const char* xr, const char* w, size_t row_bytes,
+__device__ __forceinline__ void dot_f64_range(const char* xr, const char* w, size_t row_bytes, int cb, int ce,
                                               const int (&ids)[8], int lane, double (&out)[8]) {
-    constexpr int U = 4;
+    constexpr int U = 2;
     constexpr int EPC = MODE == MODE_BF16 ? 8 : 4;  // elements per 16-byte chunk
     double acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0;
-    const int nch = (int)(row_bytes / 16);
-    for (int c0 = 0; c0 < nch; c0 += kWave * U) {
-        uint4 xv[U];
+    for (int c0 = cb; c0 < ce; c0 += kWave * U) {
+        uint4 xv[U], wv[8][U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * kWave + lane;
-            xv[u] = c < nch ? *(const uint4*)(xr + (size_t)c * 16) : make_uint4(0, 0, 0, 0);
+            xv[u] = c < ce ? *(const uint4*)(xr + (size_t)c * 16) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                wv[i][u] = (ids[i] >= 0 && c < ce) ? *(const uint4*)(w + (size_t)ids[i] * row_bytes + (size_t)c * 16)
+                                                   : make_uint4(0, 0, 0, 0);
         }
-#pragma unroll 1
-        for (int ib = 0; ib < 8; ib += 4) {
-            if (ids[ib] < 0) break;
-            uint4 wv[4][U];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int c = c0 + u * kWave + lane;
-                    wv[i][u] = (ids[ib + i] >= 0 && c < nch)
-                                   ? *(const uint4*)(w + (size_t)ids[ib + i] * row_bytes + (size_t)c * 16)
-                                   : make_uint4(0, 0, 0, 0);
+            for (int u = 0; u < U; ++u) {
+                if constexpr (MODE == MODE_BF16) {
+                    const uint16_t* xs = (const uint16_t*)&xv[u];
+                    const uint16_t* ws = (const uint16_t*)&wv[i][u];
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e)
+                        acc[i] += (double)bf16_to_f32(xs[e]) * (double)bf16_to_f32(ws[e]);
+                } else {
+                    const float* xs = (const float*)&xv[u];
+                    const float* ws = (const float*)&wv[i][u];
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) acc[i] += (double)xs[e] * (double)ws[e];
                 }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    if constexpr (MODE == MODE_BF16) {
-                        const uint16_t* xs = (const uint16_t*)&xv[u];
-                        const uint16_t* ws = (const uint16_t*)&wv[i][u];
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e)
-                            acc[ib + i] += (double)bf16_to_f32(xs[e]) * (double)bf16_to_f32(ws[e]);
-                    } else {
-                        const float* xs = (const float*)&xv[u];
-                        const float* ws = (const float*)&wv[i][u];
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e) acc[ib + i] += (double)xs[e] * (double)ws[e];
-                    }
-                }
-        }
+            }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) out[i] = ids[i] >= 0 ? group_sum<kWave>(acc[i]) : 0.0;
@@ -361,9 +387,9 @@ __device__ __forceinline__ void route_issue(const uint16_t* const (&src)[C::DPW]
     }
 }
 
-template <int TB, int NBLK>
+template <int TB, int NBLK, int KW>
 __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char* ring, char* dummy, int t0) {
-    using C = RouteCfg<TB, NBLK>;
+    using C = RouteCfg<TB, NBLK, KW>;
     const uint16_t* x = (const uint16_t*)p.x;
     const uint16_t* w = (const uint16_t*)p.w;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -406,9 +432,16 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
 #pragma unroll
     for (int nb = 0; nb < NBLK; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int arow = tb * 16 + r16;
-    const int c0 = ks * 8 + 2 * q;  // logical chunks c0, c0+1 of this lane's A and B fragments
-    const int pa0 = ((c0 ^ (arow & C::SWZ)) << 4), pa1 = (((c0 + 1) ^ (arow & C::SWZ)) << 4);
-    const int pb0 = ((c0 ^ (r16 & C::SWZ)) << 4), pb1 = (((c0 + 1) ^ (r16 & C::SWZ)) << 4);
+    // logical chunks c0 .. c0+2KW-1 of this lane's A and B fragments: the k
+    // index of MFMA u, lane group q, element j is chunk c0+u, element j
+    constexpr int NU = 2 * KW;
+    const int c0 = ks * 8 * KW + NU * q;
+    int pa[NU], pb[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+        pa[u] = ((c0 + u) ^ (arow & C::SWZ)) << 4;
+        pb[u] = ((c0 + u) ^ (r16 & C::SWZ)) << 4;
+    }
 
     // prologue: super-chunks 0 .. NSLOT-2 in flight
 #pragma unroll
@@ -425,16 +458,19 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
         if (fill < nsc) route_issue<C>(src, lcol, ldst, real, ring0, dummy0, d, fill, slot == 0 ? C::NSLOT - 1 : slot - 1);
         const char* base = ring + slot * C::SLOT;
         const int col0 = c * C::KC + c0 * 8;
-        uint4 a0 = *(const uint4*)(base + arow * C::ROWB + pa0);
-        uint4 a1 = *(const uint4*)(base + arow * C::ROWB + pa1);
-        if (col0 >= d) a0 = make_uint4(0, 0, 0, 0);
-        if (col0 + 8 >= d) a1 = make_uint4(0, 0, 0, 0);
+        uint4 a[NU];
 #pragma unroll
-        for (int nb = 0; nb < NBLK; ++nb) {
-            const char* bp = base + (C::BT + nb * 16 + r16) * C::ROWB;
-            acc[nb] = mfma16(a0, *(const uint4*)(bp + pb0), acc[nb]);
-            acc[nb] = mfma16(a1, *(const uint4*)(bp + pb1), acc[nb]);
+        for (int u = 0; u < NU; ++u) {
+            a[u] = *(const uint4*)(base + arow * C::ROWB + pa[u]);
+            if (col0 + 8 * u >= d) a[u] = make_uint4(0, 0, 0, 0);
         }
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+#pragma unroll
+            for (int nb = 0; nb < NBLK; ++nb) {
+                const char* bp = base + (C::BT + nb * 16 + r16) * C::ROWB;
+                acc[nb] = mfma16(a[u], *(const uint4*)(bp + pb[u]), acc[nb]);
+            }
         slot = slot + 1 == C::NSLOT ? 0 : slot + 1;
     }
     wait_vmcnt<0>();
@@ -465,10 +501,10 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
     }
 }
 
-template <int MODE, int TB, int NBLK>
+template <int MODE, int TB, int NBLK, int KW>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     extern __shared__ __align__(16) char smem[];
-    const RouteSmem sm = route_smem<MODE, TB, NBLK>(p.E);
+    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(p.E);
     constexpr int BT = 16 * TB;
     constexpr int TPW = BT / 4;  // tokens per wave in the selection steps
     static_assert(TPW * 32 <= 512, "pick area of a wave");
@@ -492,7 +528,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
 
     // ---- 1. logits tile
     if constexpr (MODE == MODE_BF16) {
-        logits_bf16<TB, NBLK>(p, zs, ring, dummy, t0);
+        logits_bf16<TB, NBLK, KW>(p, zs, ring, dummy, t0);
     } else if constexpr (MODE == MODE_F32) {
         const float* x = (const float*)p.x;
         const float* w = (const float*)p.w;
@@ -531,31 +567,63 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
         SelectCtx c{zs, sm.zstride, cl, e2g_s, fl_count + wave, fl_tok + wave * 16, fl_thr + wave * 16,
                     t0, wave * TPW, MODE != MODE_LOGITS_IN};
         switch (S) {
-            case 1: select_tokens<1, TPW>(p, c, lane); break;
-            case 2: select_tokens<2, TPW>(p, c, lane); break;
-            case 4: select_tokens<4, TPW>(p, c, lane); break;
-            case 8: select_tokens<8, TPW>(p, c, lane); break;
-            default: select_tokens<16, TPW>(p, c, lane); break;
+            case 1: select_tokens_v<1, TPW>(p, c, lane); break;
+            case 2: select_tokens_v<2, TPW>(p, c, lane); break;
+            case 4: select_tokens_v<4, TPW>(p, c, lane); break;
+            case 8: select_tokens_v<8, TPW>(p, c, lane); break;
+            default: select_tokens_v<16, TPW>(p, c, lane); break;
         }
     }
 
-    // ---- 3. float64 decision for this wave's queued tokens (one wave per token)
+    // ---- 3. float64 decision for the workgroup's queued tokens
     // Only experts whose fp32 logit is within the gap of the k-th value can be
     // in the exact top-k (the fp32 logits are far more accurate than the gap);
     // they are recomputed from exact float64 products and the picks are taken
-    // among them. The queue is the wave's own, so no workgroup barrier.
+    // among them. The queued tokens are spread over the four waves: a lone
+    // token gets all four, two get two each, more get one each. The waves of a
+    // team each sum the products of their share of the row into their own LDS
+    // area; the team's first wave adds the shares in wave order and decides.
     if constexpr (MODE != MODE_LOGITS_IN) {
-        lds_reads_done();
-        const int nf = fl_count[wave];
+        __syncthreads();  // every wave's queue is complete
+        const int q0 = fl_count[0], q1 = fl_count[1], q2 = fl_count[2], q3 = fl_count[3];
+        const int nq = q0 + q1 + q2 + q3;
+        const int sp = nq >= 3 ? 1 : (nq == 2 ? 2 : 4);  // waves per token
+        const int team = wave / sp, mate = wave % sp;
         const size_t xrow_bytes = (size_t)p.d * (MODE == MODE_BF16 ? 2 : 4);
-        // wave area: candidate ids [0, 1 KB), their exact logits (up to 32) at
-        // 1 KB, the pick list at 1280 B (16 packed picks, 16 logits)
-        double* cz = (double*)(cl + 256);
+        const int nch = (int)(xrow_bytes / 16);
+        const int qc = ceil_div(nch, sp);
+        const int cb = min(nch, mate * qc), ce = min(nch, cb + qc);
+        // wave area: candidate ids [0, 1 KB), partial then exact logits of the
+        // candidates (up to 32) at 1 KB, the pick list at 1280 B (16 packed
+        // picks, 16 logits), the second buffer of partial logits at 1536 B
         int* pk3 = cl + 320;
         double* pv3 = (double*)(cl + 336);
-        for (int f = 0; f < nf; ++f) {
-            const int tl = fl_tok[wave * 16 + f];
-            const float thr = fl_thr[wave * 16 + f];
+        const int* area0 = (const int*)(smem + sm.zs_bytes + sm.flag_bytes);
+        int parity = 0;
+        for (int f0 = 0; f0 < nq; f0 += 4 / sp, parity ^= 1) {
+            const int f = f0 + team;
+            const bool active = f < nq;
+            const int zoff = parity ? 384 : 256;  // int offset of this round's partials
+            double* cz = (double*)(cl + zoff);
+            int tl = 0;
+            float thr = 0.f;
+            if (active) {
+                int qw = 0, pos = f;
+                if (pos >= q0) {
+                    pos -= q0;
+                    qw = 1;
+                    if (pos >= q1) {
+                        pos -= q1;
+                        qw = 2;
+                        if (pos >= q2) {
+                            pos -= q2;
+                            qw = 3;
+                        }
+                    }
+                }
+                tl = fl_tok[qw * 16 + pos];
+                thr = fl_thr[qw * 16 + pos];
+            }
             const int t = t0 + tl;
             const char* xr = (const char*)p.x + (size_t)t * xrow_bytes;
             float fz[4];
@@ -564,9 +632,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
             for (int j = 0; j < 4; ++j) {
                 const int e = lane + kWave * j;
                 fz[j] = e < E ? zs[tl * sm.zstride + e] : -INFINITY;
-                cand[j] = e < E && fz[j] >= thr;
+                cand[j] = active && e < E && fz[j] >= thr;
             }
-            // candidate list (ascending expert id) in this wave's LDS area
+            // candidate list (ascending expert id): the waves of a team build
+            // the same list, each in its own area
             int nc = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -575,27 +644,43 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
                 nc += __popcll(m);
             }
             lds_reads_done();
-            double top;
-            float sc = 0.f;  // this lane's softmax terms of candidates
-            if (nc <= 32) {
-                // exact logits of the candidates into LDS, eight at a time
+            const bool shared = active && nc <= 32;
+            // the deciding lane's bias, loaded before the products so that its
+            // latency hides behind theirs
+            const double bmid = (shared && mate == 0 && lane < nc && p.bias) ? (double)p.bias[cl[lane]] : 0.0;
+            if (shared) {
                 for (int b0 = 0; b0 < nc; b0 += 8) {
                     int ids[8];
                     double z[8];
 #pragma unroll
                     for (int i = 0; i < 8; ++i) ids[i] = b0 + i < nc ? cl[b0 + i] : -1;
-                    dot_f64_batch<MODE>(xr, (const char*)p.w, xrow_bytes, ids, lane, z);
+                    dot_f64_range<MODE>(xr, (const char*)p.w, xrow_bytes, cb, ce, ids, lane, z);
 #pragma unroll
                     for (int i = 0; i < 8; ++i)
-                        if (lane == i && ids[i] >= 0) cz[b0 + i] = z[i] + (p.bias ? (double)p.bias[ids[i]] : 0.0);
+                        if (lane == i && ids[i] >= 0) cz[b0 + i] = z[i];
+                }
+            }
+            // the shares of every team are complete; the partials of the next
+            // round go to the other buffer, so one barrier per round suffices
+            __syncthreads();
+            if (!active || mate != 0) continue;
+            double top;
+            float sc = 0.f;  // this lane's softmax terms of candidates
+            if (shared) {
+                // lane i completes candidate i, then ranks it among all
+                // candidates (ties: lower id); the ranks are a permutation, the
+                // first k are the picks
+                double mz = -INFINITY;
+                int mid = 0;
+                if (lane < nc) {
+                    double zsum = 0.0;
+                    for (int w = 0; w < sp; ++w) zsum += ((const double*)(area0 + (wave + w) * 512 + zoff))[lane];
+                    mid = cl[lane];
+                    mz = zsum + bmid;
+                    cz[lane] = mz;
                 }
                 lds_reads_done();
-                // lane i ranks candidate i among all candidates (ties: lower id);
-                // the ranks are a permutation, the first k are the picks
-                double mz = -INFINITY;
                 if (lane < nc) {
-                    mz = cz[lane];
-                    const int mid = cl[lane];
                     int rank = 0;
                     for (int j = 0; j < nc; ++j) rank += better(cz[j], cl[j], mz, mid) ? 1 : 0;
                     if (rank < k) {
@@ -607,7 +692,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
                 top = pv3[0];
                 if (lane < nc) sc = __expf((float)(mz - top));
             } else {
-                // many near-equal logits: candidates stay in their experts' lanes
+                // many near-equal logits: the team's first wave takes the whole
+                // row alone, candidates stay in their experts' lanes
                 double zz[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) zz[j] = -INFINITY;
@@ -616,7 +702,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
 #pragma unroll
                     for (int i = 0; i < 8; ++i) ids[i] = b0 + i < nc ? cl[b0 + i] : -1;
                     double z[8];
-                    dot_f64_batch<MODE>(xr, (const char*)p.w, xrow_bytes, ids, lane, z);
+                    dot_f64_range<MODE>(xr, (const char*)p.w, xrow_bytes, 0, nch, ids, lane, z);
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
                         if (ids[i] < 0) continue;
@@ -669,13 +755,22 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     }
 }
 
-template <int MODE, int TB, int NBLK>
+template <int MODE, int TB, int NBLK, int KW = 1>
 hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
-    const RouteSmem sm = route_smem<MODE, TB, NBLK>(a.E);
-    auto kern = route_kernel<MODE, TB, NBLK>;
-    hipError_t err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)sm.total());
+    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(a.E);
+    auto kern = route_kernel<MODE, TB, NBLK, KW>;
+    // the kernel's dynamic LDS limit is raised to the whole 160 KiB once per
+    // device (the attribute only permits; each launch asks for what it uses)
+    static std::atomic<uint32_t> raised{0};  // bit d: done on device d < 32
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
+    const uint32_t bit = dev >= 0 && dev < 32 ? 1u << dev : 0u;
+    if (bit == 0u || !(raised.load(std::memory_order_acquire) & bit)) {
+        err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (err != hipSuccess) return err;
+        raised.fetch_or(bit, std::memory_order_release);
+    }
     dim3 grid(ceil_div(a.T, 16 * TB));
     hipLaunchKernelGGL(kern, grid, dim3(kRouteThreads), sm.total(), s, a);
     return hipGetLastError();
@@ -683,8 +778,15 @@ hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
 
 template <int TB>
 hipError_t launch_bf16(const RouteArgs& a, hipStream_t s) {
-    if (a.E <= 16) return launch_one<MODE_BF16, TB, 1>(a, s);
-    if (a.E <= 64) return launch_one<MODE_BF16, TB, 4>(a, s);
+    // two 64-column units per wave and copy step where two ring slots still
+    // fit (fewer barriers per byte); the decode-sized tile of 16 tokens with
+    // up to 64 experts keeps one
+    if (a.E <= 16) return launch_one<MODE_BF16, TB, 1, 2>(a, s);
+    if constexpr (TB > 1) {
+        if (a.E <= 64) return launch_one<MODE_BF16, TB, 4, 2>(a, s);
+    } else {
+        if (a.E <= 64) return launch_one<MODE_BF16, TB, 4, 1>(a, s);
+    }
     return launch_one<MODE_BF16, 4, 16>(a, s);
 }
 
