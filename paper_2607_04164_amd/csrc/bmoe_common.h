@@ -177,6 +177,10 @@ struct FfnArgs {
 size_t ffn_workspace_bytes();
 // part: 0 = both GEMMs, 1 = gate/up only, 2 = down only
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part = 0);
+// skinny path for decode-sized batches (bf16, capacity of at most 64 rows per
+// segment on average); launch_ffn takes it when ffn_skinny_fits
+bool ffn_skinny_fits(const FfnArgs& a);
+hipError_t launch_ffn_skinny(const FfnArgs& a, hipStream_t s, int part);
 
 struct CombineArgs {
     const int32_t* slot_row;

@@ -941,6 +941,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
         }
         return hipSuccess;
     }
+    if (ffn_skinny_fits(a)) return launch_ffn_skinny(a, s, part);
     const int tile = ffn_tile(a);
     if (up) {
         GemmParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up,

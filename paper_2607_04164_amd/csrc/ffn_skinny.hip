@@ -1,0 +1,212 @@
+// Skinny grouped GEMMs for decode-sized batches: the per-united-expert
+// SwiGLU FFN of Sec. 2.1 when every group holds only a few dozen rows, so the
+// layer is bound by streaming the united-expert weights, not by MFMA.
+//
+// One workgroup (4 waves) owns one segment and 64 output columns; wave w owns
+// columns n0 .. n0+15 with n0 = 64*cb + 16*w (for the fused gate/up GEMM: those
+// rows of both W_gate and W_up). The segment's rows are taken 64 at a time
+// (one pass over the weights per 64 rows). Per K-chunk of 256 columns:
+//   - the 64 activation rows (clamped to the segment) are loaded to registers
+//     and written to a swizzled LDS slot that the four waves share;
+//   - each wave loads its weight rows straight into registers in the MFMA
+//     operand layout (each load instruction reads 64 contiguous bytes of each
+//     of the wave's 16 weight rows);
+//   - 16x16x32 bf16 MFMA with the weights as the A operand and the
+//     activations as the B operand, D[weight row][row of the segment].
+// MFMA u covers columns 32u .. 32u+31 of the chunk, lane group q its columns
+// 32u + 8q .. 32u + 8q + 7 (both operands). Chunks are double-buffered in
+// registers and LDS; the loop is unrolled by two so that no register array is
+// indexed at run time, and chunks past the end hold zero activations instead
+// of branching around MFMAs.
+#include "bmoe_common.h"
+
+namespace bmoe {
+namespace {
+
+constexpr int kSkThreads = 256;
+constexpr int kSkRows = 64;                      // activation rows per pass
+constexpr int kSkKC = 256;                       // K columns per chunk
+constexpr int kSkCols = 64;                      // output columns per workgroup
+constexpr int kSkRowBytes = kSkKC * 2;           // 512 B per LDS row
+constexpr int kSkSlot = kSkRows * kSkRowBytes;   // 32 KiB per chunk
+constexpr int kSkXLoads = kSkSlot / 16 / kSkThreads;  // 16-byte activation loads per thread
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));  // native vector: stays in registers
+
+struct SkinnyParams {
+    const uint16_t* A;   // [rows_cap, K]
+    const uint16_t* B0;  // [n_seg, N, K]
+    const uint16_t* B1;  // [n_seg, N, K] (gated: W_up)
+    uint16_t* C;         // [rows_cap, N]
+    const int32_t* offsets;
+    int n_seg, rows_cap, N, K;
+};
+
+// LDS byte offset of logical 16-byte chunk c of activation row r
+__device__ __forceinline__ int sk_off(int r, int c) { return r * kSkRowBytes + ((c ^ (r & 15)) << 4); }
+
+// Chunk c of the pass's activation rows [m0, m0+64) (clamped to the segment)
+// into xs, and of the lane's weight rows into wv. Addresses past the end of a
+// row or past the last chunk are clamped to column 0 (finite values); the
+// activations of those columns are zeroed when they are written to LDS, so
+// their products vanish and no load result is touched before it is used.
+template <int NMAT>
+__device__ __forceinline__ void sk_load(const SkinnyParams& p, const uint16_t* const (&wp)[NMAT], int c, int nch,
+                                        int m0, int end, int q, v4u (&xs)[kSkXLoads], v4u (&wv)[NMAT][8]) {
+    const int K = p.K;
+    const int kc0 = min(c, nch - 1) * kSkKC;
+#pragma unroll
+    for (int j = 0; j < kSkXLoads; ++j) {
+        const int i = threadIdx.x + kSkThreads * j;
+        const int row = min(m0 + (i >> 5), end - 1);
+        int col = kc0 + (i & 31) * 8;
+        if (col >= K) col = 0;
+        xs[j] = *(const v4u*)(p.A + (size_t)row * K + col);
+    }
+    // the activations are issued before the weights: their LDS store (one
+    // chunk earlier than the weights' MFMAs) then waits only for older loads
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int mat = 0; mat < NMAT; ++mat)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int col = kc0 + u * 32 + q * 8;
+            wv[mat][u] = *(const v4u*)(wp[mat] + (col < K ? col : 0));
+        }
+}
+
+__device__ __forceinline__ void sk_store_x(const v4u (&xs)[kSkXLoads], char* slot, int c, int nch, int K) {
+    const int kc0 = c * kSkKC;
+#pragma unroll
+    for (int j = 0; j < kSkXLoads; ++j) {
+        const int i = threadIdx.x + kSkThreads * j;
+        const uint32_t keep = (c < nch && kc0 + (i & 31) * 8 < K) ? ~0u : 0u;
+        *(v4u*)(slot + sk_off(i >> 5, i & 31)) = xs[j] & keep;
+    }
+}
+
+template <int NMAT>
+__device__ __forceinline__ void sk_compute(f32x4 (&acc)[NMAT][4], const char* slot, const v4u (&wv)[NMAT][8],
+                                           int r16, int q) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        v4u xf[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) xf[nt] = *(const v4u*)(slot + sk_off(nt * 16 + r16, u * 4 + q));
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int mat = 0; mat < NMAT; ++mat)
+                acc[mat][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv[mat][u]),
+                                                                       __builtin_bit_cast(bf16x8, xf[nt]),
+                                                                       acc[mat][nt], 0, 0, 0);
+    }
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(kSkThreads, 1) void skinny_gemm_kernel(SkinnyParams p) {
+    constexpr int NMAT = GATED ? 2 : 1;
+    __shared__ __align__(16) char lds[2 * kSkSlot];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int ncb = ceil_div(p.N, kSkCols);
+    const int s = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+    if (s >= p.n_seg) return;
+    const int beg = min(max(p.offsets[s], 0), p.rows_cap);
+    const int end = min(max(p.offsets[s + 1], beg), p.rows_cap);
+    if (end <= beg) return;
+    const int K = p.K, N = p.N;
+    const int nch = ceil_div(K, kSkKC);
+    const int r16 = lane & 15, q = lane >> 4;
+    const int n0 = cb * kSkCols + wave * 16;
+    const int wrow = min(n0 + r16, N - 1);  // clamped: loads stay in bounds
+    const uint16_t* wp[NMAT];
+    wp[0] = p.B0 + ((size_t)s * N + wrow) * K;
+    if constexpr (GATED) wp[NMAT - 1] = p.B1 + ((size_t)s * N + wrow) * K;
+    char* slot0 = lds;
+    char* slot1 = lds + kSkSlot;
+
+    for (int m0 = beg; m0 < end; m0 += kSkRows) {
+        f32x4 acc[NMAT][4];
+#pragma unroll
+        for (int mat = 0; mat < NMAT; ++mat)
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) acc[mat][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // two stages: chunk c's weights are loaded two chunks ahead, its
+        // activations one chunk before they are written to LDS (a third stage
+        // measured slower)
+        v4u xs0[kSkXLoads], xs1[kSkXLoads];
+        v4u w0[NMAT][8], w1[NMAT][8];
+        sk_load<NMAT>(p, wp, 0, nch, m0, end, q, xs0, w0);
+        sk_load<NMAT>(p, wp, 1, nch, m0, end, q, xs1, w1);
+        sk_store_x(xs0, slot0, 0, nch, K);
+        __syncthreads();
+        for (int c = 0; c < nch; c += 2) {
+            sk_compute<NMAT>(acc, slot0, w0, r16, q);  // chunk c
+            sk_store_x(xs1, slot1, c + 1, nch, K);     // chunk c+1 (slot released by the last barrier)
+            sk_load<NMAT>(p, wp, c + 2, nch, m0, end, q, xs0, w0);
+            __syncthreads();
+            sk_compute<NMAT>(acc, slot1, w1, r16, q);  // chunk c+1 (zero activations past the end)
+            sk_store_x(xs0, slot0, c + 2, nch, K);     // chunk c+2
+            sk_load<NMAT>(p, wp, c + 3, nch, m0, end, q, xs1, w1);
+            __syncthreads();
+        }
+
+        // epilogue: lane holds D[weight row 4q+i][segment row r16] of every
+        // row tile nt, i.e. output columns n0+4q .. n0+4q+3 of row m0+16nt+r16
+        const int col = n0 + 4 * q;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int row = m0 + nt * 16 + r16;
+            if (row >= end) continue;
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if constexpr (GATED) v[i] = silu_mul(acc[0][nt][i], acc[NMAT - 1][nt][i]);
+                else v[i] = acc[0][nt][i];
+            }
+            uint16_t* dst = p.C + (size_t)row * N + col;
+            if (col + 3 < N) {
+                *(uint2*)dst = make_uint2(pack_bf16x2_hw(v[0], v[1]), pack_bf16x2_hw(v[2], v[3]));
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (col + i < N) dst[i] = f32_to_bf16(v[i]);
+            }
+        }
+        // the LDS slots are rewritten by the next pass
+        __syncthreads();
+    }
+}
+
+template <bool GATED>
+hipError_t launch_skinny(const SkinnyParams& sp, hipStream_t s) {
+    const int64_t blocks = (int64_t)sp.n_seg * ceil_div(sp.N, kSkCols);
+    if (blocks <= 0) return hipSuccess;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((skinny_gemm_kernel<GATED>), dim3((unsigned)blocks), dim3(kSkThreads), 0, s, sp);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool ffn_skinny_fits(const FfnArgs& a) {
+    return a.dtype == BMOE_BF16 && (int64_t)a.rows_cap <= (int64_t)kSkRows * a.n_seg;
+}
+
+hipError_t launch_ffn_skinny(const FfnArgs& a, hipStream_t s, int part) {
+    const bool up = part != 2, down = part != 1;
+    if (up) {
+        SkinnyParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up, (uint16_t*)a.h,
+                        a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
+        hipError_t e = launch_skinny<true>(g1, s);
+        if (e != hipSuccess) return e;
+    }
+    if (down) {
+        SkinnyParams g2{(const uint16_t*)a.h, (const uint16_t*)a.w_down, nullptr, (uint16_t*)a.y, a.offsets,
+                        a.n_seg, a.rows_cap, a.d, a.d_ff};
+        return launch_skinny<false>(g2, s);
+    }
+    return hipSuccess;
+}
+
+}  // namespace bmoe

@@ -200,17 +200,52 @@ def test_ffn(name, seed):
         assert_close_rows(host_f32(ys), ref["y_shared"], cfg.dtype, "y_shared")
 
 
-def test_ffn_skewed_and_empty_segments():
-    """Hot/cold segment sizes (1 row .. many tiles) and empty segments anywhere."""
+@pytest.mark.parametrize("spare", [5, 200], ids=["skinny", "tile128"])
+def test_ffn_skewed_and_empty_segments(spare):
+    """Hot/cold segment sizes (1 row .. many tiles) and empty segments anywhere.
+
+    With 5 spare rows the capacity averages under 64 rows per segment, which
+    selects the skinny kernels (the 300- and 129-row segments take several
+    64-row passes); with 200 spare rows the 128-row tiles run.
+    """
     r = np.random.default_rng(11)
     d, f, nseg = 256, 200, 7
     sizes = [0, 1, 300, 0, 129, 2, 0]
     offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
     N = int(offsets[-1])
-    a = W.f32_to_bf16_bits(r.standard_normal((N + 5, d)).astype(np.float32))
+    a = W.f32_to_bf16_bits(r.standard_normal((N + spare, d)).astype(np.float32))
     wg = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / 16).astype(np.float32))
     wu = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / 16).astype(np.float32))
     wd = W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / 16).astype(np.float32))
+    ref_y = oracle.ffn(offsets, W.bf16_bits_to_f32(a), *(W.bf16_bits_to_f32(t) for t in (wg, wu, wd)))
+    yg, _ = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
+                  dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"))
+    torch.cuda.synchronize()
+    assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
+
+
+SKINNY_FFN = [
+    # (segment sizes, spare rows, d, d_ff): capacity <= 64 rows per segment on
+    # average selects the skinny kernels
+    ((9, 14, 55, 59, 45, 32, 27, 62), 81, 2048, 1408),  # decode-shaped layer (G=8, top-6 of 64 tokens)
+    ((3, 0, 70, 1), 2, 328, 136),     # K tails (328 = 256 + 72, 136), N tails (136 = 2*64 + 8), two passes
+    ((64, 65, 1, 0, 120), 0, 264, 72),  # exact and ragged 64-row passes, 72 = 64 + 8 columns
+]
+
+
+@pytest.mark.parametrize("sizes,spare,d,f", SKINNY_FFN, ids=[f"seg{len(c[0])}-d{c[2]}-f{c[3]}" for c in SKINNY_FFN])
+def test_ffn_skinny_paths(sizes, spare, d, f):
+    """Decode-sized segments: skinny weight-streaming kernels against the oracle."""
+    r = np.random.default_rng(len(sizes) * 1000 + d)
+    nseg = len(sizes)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N = int(offsets[-1])
+    cap = N + spare
+    assert cap <= 64 * nseg
+    a = W.f32_to_bf16_bits(r.standard_normal((cap, d)).astype(np.float32))
+    wg = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32))
+    wu = W.f32_to_bf16_bits((r.standard_normal((nseg, f, d)) / np.sqrt(d)).astype(np.float32))
+    wd = W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / np.sqrt(f)).astype(np.float32))
     ref_y = oracle.ffn(offsets, W.bf16_bits_to_f32(a), *(W.bf16_bits_to_f32(t) for t in (wg, wu, wd)))
     yg, _ = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"))
