@@ -38,8 +38,8 @@ VALU_F32_PEAK_TFLOPS = 157.3
 # --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
 # all of them). Valid only for the kernel sources they were taken with.
 TRAFFIC_RECORDS = {
-    "mixtral": {"src_sha1": "de9c2ffe46d9b8b6f1cca02f13b4021d7ba5b7ac",
-                "fetch_kib": 1702291.4, "write_kib": 312072.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "mixtral": {"src_sha1": "2639d3c2ef0b9ab731fbdf4c4e10549997f0d714",
+                "fetch_kib": 1732595.4, "write_kib": 312072.0, "fetch_scale": 2.0, "write_scale": 1.0,
                 "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
 }
 TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
