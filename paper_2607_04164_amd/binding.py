@@ -300,6 +300,11 @@ class LayerForward:
     weights: dict with w_router [E,d], bias [E] (float or None), e2g [E] int32,
     w_gate/w_up [G,d_ff,d], w_down [G,d,d_ff], and optionally w_gate_sh/w_up_sh
     [1,d_ff_shared,d], w_down_sh [1,d,d_ff_shared] (all device tensors).
+
+    Weights, buffers and workspaces are checked once here and their pointers
+    marshalled once; a call checks only x and looks up the current stream, so
+    the host cost per call stays a few microseconds (decode-sized layers take
+    less GPU time than the checks of the free functions).
     """
 
     def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True):
@@ -328,40 +333,91 @@ class LayerForward:
             self.bufs["h_sh"] = _empty((max(T, 1), desc.d_ff_shared), dt, device)
             self.bufs["y_sh"] = _empty((max(T, 1), d), dt, device)
             self.sh_offsets = torch.tensor([0, T], dtype=torch.int32, device=device)
+        self._plan()
+
+    def _plan(self):
+        """Checks every fixed tensor and marshals the fixed arguments of each call."""
+        desc, w, b = self.desc, self.w, self.bufs
+        T, k, d, G, E, f = desc.T, desc.top_k, desc.d, desc.G, desc.E, desc.d_ff
+        dt = desc.torch_dtype
+        dtype = BMOE_BF16 if dt == torch.bfloat16 else BMOE_F32
+        _dev(w["w_router"], "w_router", dt, (E, d))
+        _dev(w["e2g"], "e2g", torch.int32, (E,))
+        if w.get("bias") is not None:
+            _dev(w["bias"], "bias", torch.float32, (E,))
+        _dev(w["w_gate"], "w_gate", dt, (G, f, d))
+        _dev(w["w_up"], "w_up", dt, (G, f, d))
+        _dev(w["w_down"], "w_down", dt, (G, d, f))
+        ptr = lambda t: None if t is None else t.data_ptr()
+        wsp, wsn = (ptr(self.ffn_ws), self.ffn_ws.numel()) if self.ffn_ws is not None else (None, 0)
+        self._lib = load_library()
+        self._desc_ref = ctypes.byref(desc)
+        self._xshape, self._dt = (T, d), dt
+        r, dp = b["route"], b["dispatch"]
+        self._route_args = (ptr(w["w_router"]), ptr(w.get("bias")), None, ptr(w["e2g"]), ptr(r["topk_idx"]),
+                            ptr(r["topk_w"]), ptr(r["slot_group"]), ptr(r["slot_gate"]), None)
+        self._dispatch_args = (ptr(dp["counts"]), ptr(dp["offsets"]), ptr(dp["perm_token"]), ptr(dp["slot_row"]),
+                               ptr(dp["x_perm"]), ptr(self.ws), self.ws.numel())
+        rows = max(T * k, 1)
+        self._gate_up_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(dp["x_perm"]), ptr(w["w_gate"]),
+                              ptr(w["w_up"]), ptr(b["h"]), wsp, wsn)
+        self._down_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(b["h"]), ptr(w["w_down"]), ptr(b["y"]),
+                           wsp, wsn)
+        self._ffn_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(dp["x_perm"]), ptr(w["w_gate"]),
+                          ptr(w["w_up"]), ptr(w["w_down"]), ptr(b["h"]), ptr(b["y"]), wsp, wsn)
+        self._combine_args = (ptr(dp["slot_row"]), ptr(r["slot_gate"]), ptr(b["y"]),
+                              ptr(b["y_sh"]) if desc.d_ff_shared else None, ptr(b["out"]))
+        if desc.d_ff_shared:
+            fs = desc.d_ff_shared
+            _dev(w["w_gate_sh"], "w_gate_sh", dt, (1, fs, d))
+            _dev(w["w_up_sh"], "w_up_sh", dt, (1, fs, d))
+            _dev(w["w_down_sh"], "w_down_sh", dt, (1, d, fs))
+            self._shared_args = (dtype, 1, T, d, fs, ptr(self.sh_offsets), ptr(w["w_gate_sh"]),
+                                 ptr(w["w_up_sh"]), ptr(w["w_down_sh"]), ptr(b["h_sh"]), ptr(b["y_sh"]), wsp, wsn)
+
+    def _x(self, x) -> int:
+        if not (isinstance(x, torch.Tensor) and x.is_cuda and x.dtype == self._dt
+                and tuple(x.shape) == self._xshape and x.is_contiguous()):
+            _dev(x, "x", self._dt, self._xshape)
+        return x.data_ptr()
+
+    @staticmethod
+    def _s(stream) -> int:
+        return (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
 
     def route(self, x, stream=None):
-        w = self.w
-        return route(self.desc, x, w["w_router"], w.get("bias"), w["e2g"], out=self.bufs["route"],
-                     stream=stream)
+        _check(self._lib.brownout_moe_route(self._desc_ref, self._x(x), *self._route_args[:2], None,
+                                            *self._route_args[3:], self._s(stream)), "brownout_moe_route")
+        return self.bufs["route"]
 
     def dispatch(self, x, stream=None):
-        return dispatch(self.desc, self.bufs["route"]["slot_group"], x, self.ws,
-                        out=self.bufs["dispatch"], stream=stream)
+        _check(self._lib.brownout_moe_dispatch(self._desc_ref, self.bufs["route"]["slot_group"].data_ptr(),
+                                               self._x(x), *self._dispatch_args, self._s(stream)),
+               "brownout_moe_dispatch")
+        return self.bufs["dispatch"]
 
     def ffn(self, stream=None):
-        w = self.w
-        return ffn(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
-                   w["w_up"], w["w_down"], h=self.bufs["h"], y=self.bufs["y"], workspace=self.ffn_ws,
-                   stream=stream)
+        _check(self._lib.brownout_moe_ffn(*self._ffn_args, self._s(stream)), "brownout_moe_ffn")
+        return self.bufs["y"], self.bufs["h"]
 
     def ffn_gate_up(self, stream=None):
-        w = self.w
-        return ffn_gate_up(self.bufs["dispatch"]["offsets"], self.bufs["dispatch"]["x_perm"], w["w_gate"],
-                           w["w_up"], h=self.bufs["h"], workspace=self.ffn_ws, stream=stream)
+        _check(self._lib.brownout_moe_ffn_gate_up(*self._gate_up_args, self._s(stream)), "brownout_moe_ffn_gate_up")
+        return self.bufs["h"]
 
     def ffn_down(self, stream=None):
-        return ffn_down(self.bufs["dispatch"]["offsets"], self.bufs["h"], self.w["w_down"],
-                        y=self.bufs["y"], workspace=self.ffn_ws, stream=stream)
+        _check(self._lib.brownout_moe_ffn_down(*self._down_args, self._s(stream)), "brownout_moe_ffn_down")
+        return self.bufs["y"]
 
     def shared(self, x, stream=None):
-        w = self.w
-        return ffn(self.sh_offsets, x, w["w_gate_sh"], w["w_up_sh"], w["w_down_sh"],
-                   h=self.bufs["h_sh"], y=self.bufs["y_sh"], workspace=self.ffn_ws, stream=stream)
+        self._x(x)  # the shared experts read x in token order: the layer's own input
+        a = self._shared_args
+        _check(self._lib.brownout_moe_ffn(*a[:6], x.data_ptr(), *a[6:], self._s(stream)), "brownout_moe_ffn")
+        return self.bufs["y_sh"], self.bufs["h_sh"]
 
     def combine(self, stream=None):
-        y_sh = self.bufs["y_sh"] if self.desc.d_ff_shared else None
-        return combine(self.desc, self.bufs["dispatch"]["slot_row"], self.bufs["route"]["slot_gate"],
-                       self.bufs["y"], y_sh, out=self.bufs["out"], stream=stream)
+        _check(self._lib.brownout_moe_combine(self._desc_ref, *self._combine_args, self._s(stream)),
+               "brownout_moe_combine")
+        return self.bufs["out"]
 
     def __call__(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         self.route(x, stream)
