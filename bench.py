@@ -70,6 +70,9 @@ WORKLOAD_TEXT = {
              "d_ff=1408, bf16, Zipf(1.5)",
     "decode": "decode-batch grouped MoE layer: T=64, d=2048, E=64, top-6, G=8, d_ff=1408, bf16, Zipf(1.2)",
     "tiny": "tiny fp32 grouped MoE layer: T=64, d=256, E=8, top-2, G=4, d_ff=512, Zipf(1.2)",
+    "partial": "fine-grained MoE layer under partial brownout at threshold 0.4 (hot experts keep their own "
+               "FFN, cold experts go to their united expert): T=8192, d=2048, E=60, top-4, G=15, d_ff=1408, "
+               "bf16, Zipf(1.2)",
 }
 
 
@@ -80,6 +83,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="mixtral", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--theta", type=float, default=None,
+                    help="partial-brownout threshold in [0, 1] (overrides the workload's; "
+                         "0 is full brownout, 1 zero brownout)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -121,7 +127,17 @@ def time_layer(cfg, args, dev):
     from paper_2607_04164_amd import workload as W
 
     print(f"[bench] generating {cfg.name} (G={cfg.G}) seed {args.seed}", file=sys.stderr, flush=True)
-    L = W.make_layer(cfg, args.seed)
+    L0 = L = W.make_layer(cfg, args.seed)
+    seg_info = None
+    if cfg.theta is not None:
+        # partial brownout: the layer runs over the segment map (hot experts'
+        # own FFNs, then united experts) built by the library's host code
+        from paper_2607_04164_amd import brownout as BO
+        e2s, seg = BO.segment_map(W.zipf_freq(L), L.e2g, cfg.G, cfg.theta)
+        L = W.segment_layer(L, e2s, seg)
+        cfg = L.cfg
+        seg_info = {"theta": cfg.theta, "segments": len(seg),
+                    "hot_experts": [i for kind, i in seg if kind == "expert"]}
 
     def to_dev(a):
         if cfg.dtype == "bf16":
@@ -205,7 +221,7 @@ def time_layer(cfg, args, dev):
         iso_ms[s] = e0.elapsed_time(e1) / reps
     del layer, w, x
     torch.cuda.empty_cache()
-    return L, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages
+    return L0, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages
 
 
 def main():
@@ -225,10 +241,15 @@ def main():
         return
 
     cfg = W.CONFIGS[args.config]
+    if args.theta is not None:
+        if not 0.0 <= args.theta <= 1.0:
+            print("--theta must lie in [0, 1]", file=sys.stderr)
+            sys.exit(2)
+        cfg = cfg.with_(theta=args.theta)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B.load_library()
-    L, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages = time_layer(cfg, args, dev)
+    L, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages = time_layer(cfg, args, dev)
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
@@ -292,9 +313,13 @@ def main():
         "cpu_baseline": None,
     }
 
+    if seg_info is not None:
+        # G above is the united-expert count; the layer ran over the segments
+        result["config"]["partial_brownout"] = seg_info
+
     if args.compare_ungrouped and cfg.G != cfg.E:
         ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E)
-        _, ms_u, _, stages_u, _, N_u, _, _ = time_layer(ucfg, args, dev)
+        _, _, ms_u, _, stages_u, _, N_u, _, _ = time_layer(ucfg, args, dev)
         result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
                                "ms_per_step": round(ms_u, 4),
                                "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},
@@ -311,7 +336,14 @@ def cpu_baseline(L, cfg, budget_s):
     import dataclasses
 
     import oracle
-    from paper_2607_04164_amd import workload as W  # noqa: F401
+    from oracle.partial import partial_map
+    from paper_2607_04164_amd import workload as W
+
+    if cfg.theta is not None:
+        # the oracle's own segment map for partial brownout
+        e2s, seg = partial_map(W.zipf_freq(L), L.e2g, cfg.G, cfg.theta)
+        L = W.segment_layer(L, e2s, seg)
+        cfg = L.cfg
 
     # widen the bf16 storage to the float32 the oracle reads, once, outside the timing
     names = ("x", "w_router", "w_gate", "w_up", "w_down", "w_gate_sh", "w_up_sh", "w_down_sh")

@@ -31,6 +31,15 @@ Workload recipe (per layer configuration):
   experts of width ``d_ff_shared_each``; their gate/up rows and down columns
   are concatenated into one FFN of width n_shared*d_ff_shared_each, which is
   the same function as their sum.
+* Partial brownout (configurations with a threshold ``theta``): the original
+  FFN of expert e is drawn from its own generator,
+  ``default_rng([seed, 1_000_000 + e])`` (gate, up, down; same distribution
+  as the united experts), so any subset of experts can be drawn alone. The
+  calibration frequencies that pick the hot experts stand in as the Zipf law
+  of the skew bias (``zipf_freq``); the paper's calibration traces are not
+  here. ``segment_layer`` assembles the layer over a segment map (hot
+  experts' own FFNs, then united experts); the map itself comes from the
+  caller.
 """
 from __future__ import annotations
 
@@ -61,6 +70,7 @@ class LayerConfig:
     norm_topk: int = 0                   # renormalise the top-k weights to sum 1
     n_shared: int = 0                    # always-on shared experts
     d_ff_shared_each: int = 0
+    theta: Optional[float] = None        # partial-brownout threshold (None: full brownout)
 
     @property
     def d_ff_shared(self) -> int:
@@ -91,6 +101,9 @@ CONFIGS: Dict[str, LayerConfig] = {
     # decode-sized batch: a tiny, weight-streaming grouped GEMM
     "decode": LayerConfig("decode", T=64, d=2048, E=64, top_k=6, G=8, d_ff=1408,
                           dtype="bf16", zipf_s=1.2),
+    # the fine-grained layer under partial brownout at the paper's threshold 0.4
+    "partial": LayerConfig("partial", T=8192, d=2048, E=60, top_k=4, G=15, d_ff=1408,
+                           dtype="bf16", zipf_s=1.2, theta=0.4),
 }
 
 
@@ -229,3 +242,29 @@ def make_layer(cfg: LayerConfig, seed: int, *, with_weights: bool = True) -> Lay
               _normal(rng, (1, fs, d), wstd, cfg.dtype),
               _normal(rng, (1, d, fs), wstd, cfg.dtype))
     return Layer(cfg, seed, e2g, bias, x, w_router, w_gate, w_up, w_down, *sh)
+
+
+def zipf_freq(L: Layer) -> np.ndarray:
+    """The Zipf law behind the skew bias: the stand-in calibration frequencies."""
+    q = np.exp(L.bias.astype(np.float64))
+    return q / q.sum()
+
+
+def expert_weights(L: Layer, e: int):
+    """Original FFN of expert e: (w_gate [d_ff, d], w_up [d_ff, d], w_down [d, d_ff])."""
+    cfg = L.cfg
+    rng = np.random.default_rng([L.seed, 1_000_000 + int(e)])
+    wstd = 1.0 / math.sqrt(cfg.d)
+    return (_normal(rng, (cfg.d_ff, cfg.d), wstd, cfg.dtype),
+            _normal(rng, (cfg.d_ff, cfg.d), wstd, cfg.dtype),
+            _normal(rng, (cfg.d, cfg.d_ff), wstd, cfg.dtype))
+
+
+def segment_layer(L: Layer, e2s: np.ndarray, segments) -> Layer:
+    """The layer over a segment map: segment s is ("expert", e) with expert e's
+    original FFN or ("united", g) with united expert g; e2s replaces the map."""
+    parts = [expert_weights(L, i) if kind == "expert" else (L.w_gate[i], L.w_up[i], L.w_down[i])
+             for kind, i in segments]
+    wg, wu, wd = (np.stack([p[j] for p in parts]) for j in range(3))
+    cfg = L.cfg.with_(G=len(segments))
+    return dataclasses.replace(L, cfg=cfg, e2g=np.asarray(e2s, dtype=np.int32), w_gate=wg, w_up=wu, w_down=wd)

@@ -17,9 +17,11 @@ import pytest
 import torch
 
 import oracle
+from oracle.partial import partial_map
 from gpu_util import (TOL, assert_close_rows, assert_gates, desc_of, dev_tensor, device_weights,
                       group_boundary_tokens, host_f32, to_storage)
 from paper_2607_04164_amd import binding as B
+from paper_2607_04164_amd import brownout as BO
 from paper_2607_04164_amd import workload as W
 
 pytestmark = pytest.mark.gpu
@@ -471,14 +473,35 @@ def test_token_order_invariance():
 # ---------------------------------------------------------------------------
 # full-size workloads: integers in full, floats on sampled tokens
 
-@functools.lru_cache(maxsize=1)
+def partial_layer(L):
+    """The layer over the partial-brownout segment map of its threshold; the
+    library's map builder must agree with the oracle's."""
+    cfg = L.cfg
+    e2s, seg = BO.segment_map(W.zipf_freq(L), L.e2g, cfg.G, cfg.theta)
+    e2s_o, seg_o = partial_map(W.zipf_freq(L), L.e2g, cfg.G, cfg.theta)
+    assert np.array_equal(e2s, e2s_o) and seg == seg_o
+    return W.segment_layer(L, e2s, seg)
+
+
 def full_case(name):
     cfg = W.CONFIGS[name]
     L = W.make_layer(cfg, 0)
-    return L
+    return partial_layer(L) if cfg.theta is not None else L
 
 
-@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral"])
+@pytest.mark.parametrize("theta", [0.0, 0.6, 0.9, 1.0])
+def test_partial_brownout_layer(theta):
+    """Hot experts on their own FFN, cold ones on their united expert: the
+    whole layer over the segment map (theta 0: full brownout, 1: zero
+    brownout with all 60 original experts)."""
+    cfg = W.CONFIGS["partial"].with_(name="partial-s", T=300, d=256, d_ff=192, theta=theta)
+    PL = partial_layer(W.make_layer(cfg, 1))
+    ref = oracle.layer(PL, want_intermediates=True)
+    layer, out = run_layer(PL)
+    check_layer(PL, ref, layer, out)
+
+
+@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral", "partial"])
 def test_full_size_sampled(name):
     L = full_case(name)
     cfg = L.cfg
