@@ -120,8 +120,10 @@ def copy_probe(mib: int, reps: int = 10):
 
 def time_layer(cfg, args, dev):
     """Builds the seeded layer on the device and times args.steps full forwards
-    after args.warmup untimed ones. Returns the host layer, wall ms per step,
-    per-stage event ms, the row count N, the group row counts and the stages."""
+    after args.warmup untimed ones. Returns the host layer, the partial-brownout
+    segment summary (or None), wall ms per step, the dominant kernel's event
+    ms, per-stage event ms in the steps, alone and (HBM stages) with cold
+    caches, the row count N, the group row counts and the stages."""
     import torch
     from paper_2607_04164_amd import binding as B
     from paper_2607_04164_amd import workload as W
@@ -219,9 +221,27 @@ def time_layer(cfg, args, dev):
         e1.record()
         torch.cuda.synchronize()
         iso_ms[s] = e0.elapsed_time(e1) / reps
+    # the HBM-bound stages once more with cold caches: before each launch a
+    # read pass over 1 GiB evicts L2 and the 256 MB MALL (a read, so no dirty
+    # lines are left to be written back inside the timed launch)
+    cold_ms = {}
+    flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+    flush.fill_(1)
+    for s in stages:
+        if s.startswith("ffn") or s == "shared_ffn":
+            continue
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+        for e0, e1 in evs:
+            flush.sum()
+            e0.record()
+            calls[s]()
+            e1.record()
+        torch.cuda.synchronize()
+        cold_ms[s] = float(np.median([a.elapsed_time(b) for a, b in evs]))
+    del flush
     del layer, w, x
     torch.cuda.empty_cache()
-    return L0, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages
+    return L0, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
 
 
 def main():
@@ -249,7 +269,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B.load_library()
-    L, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, N, counts, stages = time_layer(cfg, args, dev)
+    L, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = time_layer(cfg, args, dev)
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
@@ -270,9 +290,12 @@ def main():
         ms = iso_ms[st_name]
         if kind == "hbm":
             rate = amount / (ms * 1e-3) / 1e9
+            cold = amount / (cold_ms[st_name] * 1e-3) / 1e9
             stage_out[st_name] = {"us": round(ms * 1e3, 2), "in_step_us": round(per_stage_ms[st_name] * 1e3, 2),
                                   "bytes": int(amount), "GB_s": round(rate, 1),
-                                  "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+                                  "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4),
+                                  "cold_us": round(cold_ms[st_name] * 1e3, 2), "cold_GB_s": round(cold, 1),
+                                  "cold_frac_of_hbm_peak": round(cold / HBM_PEAK_GBS, 4)}
         else:
             peak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
             rate = amount / (ms * 1e-3) / 1e12
@@ -319,7 +342,7 @@ def main():
 
     if args.compare_ungrouped and cfg.G != cfg.E:
         ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E)
-        _, _, ms_u, _, stages_u, _, N_u, _, _ = time_layer(ucfg, args, dev)
+        _, _, ms_u, _, stages_u, _, _, N_u, _, _ = time_layer(ucfg, args, dev)
         result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
                                "ms_per_step": round(ms_u, 4),
                                "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},

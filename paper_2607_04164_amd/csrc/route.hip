@@ -35,6 +35,7 @@ namespace {
 constexpr int kRouteThreads = 256;
 constexpr float kGap = BMOE_ROUTE_RECHECK_GAP;
 constexpr int kMaxK = BMOE_MAX_TOPK;
+static_assert(BMOE_MAX_EXPERTS <= kRouteThreads, "one map entry per thread");
 
 enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2 };
 
@@ -431,6 +432,13 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
     f32x4 acc[NBLK];
 #pragma unroll
     for (int nb = 0; nb < NBLK; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the bias of this lane's logit columns, in flight during the copies
+    float bz[NBLK];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+        const int e = nb * 16 + r16;
+        bz[nb] = (p.bias && e < E) ? p.bias[e] : 0.f;
+    }
     const int arow = tb * 16 + r16;
     // logical chunks c0 .. c0+2KW-1 of this lane's A and B fragments: the k
     // index of MFMA u, lane group q, element j is chunk c0+u, element j
@@ -496,7 +504,7 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
                 const int tl = tb * 16 + 4 * q + i;
                 for (int kk = 1; kk < KS; ++kk) v += part[((size_t)(kk - 1) * BT + tl) * EP + nb * 16 + r16];
                 const int e = nb * 16 + r16;
-                if (e < E) zs[tl * (EP + 1) + e] = v + (p.bias ? p.bias[e] : 0.f);
+                if (e < E) zs[tl * (EP + 1) + e] = v + bz[nb];
             }
     }
 }
@@ -521,10 +529,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     const int T = p.T, E = p.E, k = p.k;
     int* e2g_s = (int*)(smem + sm.zs_bytes + 1024);  // map, invalid entries -> -1
     if (tid < 4) fl_count[tid] = 0;
-    for (int i = tid; i < E; i += kRouteThreads) {
-        const int g = p.e2g[i];
-        e2g_s[i] = (g >= 0 && g < p.G) ? g : -1;
-    }
+    // the map entry of expert tid (E <= the thread count), loaded before the
+    // logits' copies are issued and written to LDS after them, so that its
+    // latency does not delay the first copy
+    const int g_in = tid < E ? p.e2g[tid] : -1;
 
     // ---- 1. logits tile
     if constexpr (MODE == MODE_BF16) {
@@ -548,6 +556,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
             zs[tl * sm.zstride + e] = p.logits_in[(size_t)t * E + e];
         }
     }
+    if (tid < E) e2g_s[tid] = (g_in >= 0 && g_in < p.G) ? g_in : -1;
     __syncthreads();
     if (p.logits_out) {
         for (int i = tid; i < BT * E; i += kRouteThreads) {
