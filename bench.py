@@ -83,6 +83,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="mixtral", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--share", default=None, metavar="tpP|epP",
+                    help="one GPU's share of the layer sharded over P GPUs: tpP times rank --share-rank's "
+                         "tensor-parallel slice (d_ff/P hidden columns; route and dispatch replicated); epP "
+                         "also times each rank's grouped FFN over its block of united experts")
+    ap.add_argument("--share-rank", type=int, default=0)
     ap.add_argument("--theta", type=float, default=None,
                     help="partial-brownout threshold in [0, 1] (overrides the workload's; "
                          "0 is full brownout, 1 zero brownout)")
@@ -140,6 +145,10 @@ def time_layer(cfg, args, dev):
         cfg = L.cfg
         seg_info = {"theta": cfg.theta, "segments": len(seg),
                     "hot_experts": [i for kind, i in seg if kind == "expert"]}
+    share = parse_share(args.share)
+    if share and share[0] == "tp":
+        L = W.tp_share(L, share[1], args.share_rank)
+        cfg = L.cfg
 
     def to_dev(a):
         if cfg.dtype == "bf16":
@@ -221,6 +230,34 @@ def time_layer(cfg, args, dev):
         e1.record()
         torch.cuda.synchronize()
         iso_ms[s] = e0.elapsed_time(e1) / reps
+    # expert-parallel shares: each rank's grouped FFN over its block of united
+    # experts, on the rows the whole dispatch gave that block
+    ep_ms = None
+    if share and share[0] == "ep":
+        P = share[1]
+        offs = layer.bufs["dispatch"]["offsets"]
+        a, h, y = layer.bufs["dispatch"]["x_perm"], layer.bufs["h"], layer.bufs["y"]
+        ws = layer.ffn_ws
+        ep_ms = []
+        for r in range(P):
+            g0, g1 = W.ep_groups(cfg.G, P, r)
+            if g0 == g1:
+                ep_ms.append(0.0)
+                continue
+            o = offs[g0:g1 + 1]
+            wg, wu, wd = w["w_gate"][g0:g1], w["w_up"][g0:g1], w["w_down"][g0:g1]
+
+            def ffn_r():
+                B.ffn(o, a, wg, wu, wd, h=h, y=y, workspace=ws)
+            ffn_r()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(3):
+                ffn_r()
+            e1.record()
+            torch.cuda.synchronize()
+            ep_ms.append(e0.elapsed_time(e1) / 3)
     # the HBM-bound stages once more with cold caches: before each launch a
     # read pass over 1 GiB evicts L2 and the 256 MB MALL (a read, so no dirty
     # lines are left to be written back inside the timed launch)
@@ -241,7 +278,17 @@ def time_layer(cfg, args, dev):
     del flush
     del layer, w, x
     torch.cuda.empty_cache()
-    return L0, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
+    return L0, (cfg, seg_info, ep_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
+
+
+def parse_share(text):
+    """"tp8" -> ("tp", 8), "ep4" -> ("ep", 4), None -> None."""
+    if text is None:
+        return None
+    kind, num = text[:2], text[2:]
+    if kind not in ("tp", "ep") or not num.isdigit() or int(num) < 1:
+        raise SystemExit(f"--share must look like tp8 or ep4, got {text!r}")
+    return kind, int(num)
 
 
 def main():
@@ -269,7 +316,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B.load_library()
-    L, seg_info, ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = time_layer(cfg, args, dev)
+    cfg0 = cfg
+    L, (cfg, seg_info, ep_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = \
+        time_layer(cfg, args, dev)
+    share = parse_share(args.share)
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
@@ -307,7 +357,8 @@ def main():
     dms = dom_ms  # HIP events around the dominant kernel inside the timed steps
     dpeak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
     dach = damount / (dms * 1e-3) / 1e12
-    traffic = recorded_traffic(args.config)
+    # the record holds for the named workload only, not a share or another threshold
+    traffic = recorded_traffic(args.config) if share is None and args.theta is None else None
     roofline = {"kernel": "grouped_gemm_dma_kernel<gated> (brownout_moe_ffn_gate_up)",
                 "bound": "mfma" if cfg.dtype == "bf16" else "alu",
                 "achieved": round(dach, 1), "peak": dpeak, "unit": "TFLOP/s",
@@ -339,23 +390,44 @@ def main():
     if seg_info is not None:
         # G above is the united-expert count; the layer ran over the segments
         result["config"]["partial_brownout"] = seg_info
+    if share is not None:
+        kind, P = share
+        if kind == "tp":
+            # one rank's share: d_ff above is the share's; the P partial
+            # outputs would be summed across the GPUs (not timed here)
+            result["config"]["share"] = {"kind": "tensor-parallel", "P": P, "rank": args.share_rank,
+                                         "d_ff_full": cfg0.d_ff}
+        else:
+            offs = np.concatenate([[0], np.cumsum(counts)])
+            ranks = []
+            for r in range(P):
+                g0, g1 = W.ep_groups(cfg.G, P, r)
+                ranks.append({"united_experts": [g0, g1], "rows": int(offs[g1] - offs[g0]),
+                              "ffn_us": round(ep_ms[r] * 1e3, 2)})
+            result["config"]["share"] = {"kind": "expert-parallel", "P": P}
+            result["ep_ffn"] = {"ranks": ranks, "straggler_us": max(r["ffn_us"] for r in ranks),
+                                "note": "each rank's grouped FFN (gate/up + down) over its block, "
+                                        "on the rows the whole dispatch gave it; exchange not timed"}
 
-    if args.compare_ungrouped and cfg.G != cfg.E:
-        ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E)
-        _, _, ms_u, _, stages_u, _, _, N_u, _, _ = time_layer(ucfg, args, dev)
+    if args.compare_ungrouped and cfg0.G != cfg0.E:
+        # zero brownout on the same layer: every expert its own group
+        ucfg = cfg0.with_(name=cfg0.name + "-ungrouped", G=cfg0.E, theta=None)
+        uargs = argparse.Namespace(**{**vars(args), "share": None})
+        _, _, ms_u, _, stages_u, _, _, N_u, _, _ = time_layer(ucfg, uargs, dev)
         result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
                                "ms_per_step": round(ms_u, 4),
                                "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},
                                "grouped_speedup": round(ms_u / ms_step, 3)}
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(L, cfg0, share, args.share_rank, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(L, cfg, budget_s):
-    """The CPU oracle, unchanged, on a bounded sample of the same tokens."""
+def cpu_baseline(L, cfg, share, rank, budget_s):
+    """The CPU oracle, unchanged, on a bounded sample of the same tokens (of
+    the same share of the layer when it is sharded)."""
     import dataclasses
 
     import oracle
@@ -366,6 +438,9 @@ def cpu_baseline(L, cfg, budget_s):
         # the oracle's own segment map for partial brownout
         e2s, seg = partial_map(W.zipf_freq(L), L.e2g, cfg.G, cfg.theta)
         L = W.segment_layer(L, e2s, seg)
+        cfg = L.cfg
+    if share and share[0] == "tp":
+        L = W.tp_share(L, share[1], rank)
         cfg = L.cfg
 
     # widen the bf16 storage to the float32 the oracle reads, once, outside the timing

@@ -177,6 +177,9 @@ BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t*
  * are never touched). a [rows_cap, d]; w_gate, w_up [n_seg, d_ff, d];
  * w_down [n_seg, d, d_ff]; h [rows_cap, d_ff] (scratch the caller owns);
  * y [rows_cap, d]. n_seg in 1..256. bf16: MFMA, fp32 accumulation.
+ * offsets[0] need not be 0: a sub-range of segments runs alone when the
+ * caller passes offsets + s0 and the weights of segments s0.. (one rank's
+ * block of united experts under expert parallelism); other rows stay untouched.
  * The shared experts of a layer run through this call too, with n_seg = 1,
  * offsets = {0, T}, a = x.
  * workspace (optional, device memory, 256-byte aligned): NULL runs one output

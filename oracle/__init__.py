@@ -136,6 +136,7 @@ class Oracle:
         n_seg, d_ff, d = wg.shape
         assert wu.shape == wg.shape and wd.shape == (n_seg, d, d_ff)
         assert offsets.shape == (n_seg + 1,)
+        assert offsets[0] == 0, "segments start at row 0"
         N = int(offsets[-1])
         assert a.shape[1] == d and a.shape[0] >= N
         y = np.empty((N, d), np.float32)

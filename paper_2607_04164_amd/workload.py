@@ -40,6 +40,13 @@ Workload recipe (per layer configuration):
   here. ``segment_layer`` assembles the layer over a segment map (hot
   experts' own FFNs, then united experts); the map itself comes from the
   caller.
+* Shares of a multi-GPU layer on one GPU: ``tp_share`` is rank r's share
+  under tensor parallelism over P GPUs (columns r*d_ff/P .. (r+1)*d_ff/P - 1
+  of every united expert's hidden width, and the same slice of each shared
+  expert; route and dispatch are replicated, and the P partial outputs add
+  up to the layer's output); ``ep_groups`` is rank r's block of united
+  experts under expert parallelism (contiguous, sizes differing by at most
+  one). Both only select existing weights.
 """
 from __future__ import annotations
 
@@ -51,7 +58,7 @@ from typing import Dict, Optional
 import numpy as np
 
 __all__ = ["LayerConfig", "CONFIGS", "Layer", "make_layer", "bf16_round_bits",
-           "bf16_bits_to_f32", "f32_to_bf16_bits", "scaled"]
+           "bf16_bits_to_f32", "f32_to_bf16_bits", "scaled", "tp_share", "ep_groups"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -268,3 +275,34 @@ def segment_layer(L: Layer, e2s: np.ndarray, segments) -> Layer:
     wg, wu, wd = (np.stack([p[j] for p in parts]) for j in range(3))
     cfg = L.cfg.with_(G=len(segments))
     return dataclasses.replace(L, cfg=cfg, e2g=np.asarray(e2s, dtype=np.int32), w_gate=wg, w_up=wu, w_down=wd)
+
+
+def tp_share(L: Layer, P: int, r: int) -> Layer:
+    """Rank r's share of the layer under P-way tensor parallelism: hidden
+    columns [r*d_ff/P, (r+1)*d_ff/P) of every united expert and of each shared
+    expert. Same tokens, router, bias and map."""
+    cfg = L.cfg
+    if P < 1 or not 0 <= r < P or cfg.d_ff % P or (cfg.n_shared and cfg.d_ff_shared_each % P):
+        raise ValueError(f"d_ff={cfg.d_ff} (shared {cfg.d_ff_shared_each}) does not split {P} ways")
+    q = cfg.d_ff // P
+    cols = slice(r * q, (r + 1) * q)
+    kw = dict(w_gate=np.ascontiguousarray(L.w_gate[:, cols, :]),
+              w_up=np.ascontiguousarray(L.w_up[:, cols, :]),
+              w_down=np.ascontiguousarray(L.w_down[:, :, cols]))
+    ncfg = cfg.with_(name=f"{cfg.name}-tp{P}r{r}", d_ff=q)
+    if cfg.n_shared:
+        n, qs = cfg.n_shared, cfg.d_ff_shared_each // P
+        sc = slice(r * qs, (r + 1) * qs)
+        d = cfg.d
+        kw.update(w_gate_sh=np.ascontiguousarray(L.w_gate_sh.reshape(n, -1, d)[:, sc, :].reshape(1, n * qs, d)),
+                  w_up_sh=np.ascontiguousarray(L.w_up_sh.reshape(n, -1, d)[:, sc, :].reshape(1, n * qs, d)),
+                  w_down_sh=np.ascontiguousarray(L.w_down_sh.reshape(d, n, -1)[:, :, sc].reshape(1, d, n * qs)))
+        ncfg = ncfg.with_(d_ff_shared_each=qs)
+    return dataclasses.replace(L, cfg=ncfg, **kw)
+
+
+def ep_groups(G: int, P: int, r: int):
+    """Rank r's united experts [g0, g1) under P-way expert parallelism."""
+    if P < 1 or not 0 <= r < P:
+        raise ValueError("rank out of range")
+    return (r * G) // P, ((r + 1) * G) // P

@@ -483,6 +483,47 @@ def partial_layer(L):
     return W.segment_layer(L, e2s, seg)
 
 
+# ---------------------------------------------------------------------------
+# one GPU's share of a layer sharded over several GPUs
+
+@pytest.mark.parametrize("base,P,r", [("mixtral-s", 8, 0), ("mixtral-s", 8, 7), ("heavy-s", 4, 2)])
+def test_tp_share_layer(base, P, r):
+    """Rank r's tensor-parallel share (d_ff/P hidden columns of every united
+    and shared expert, route and dispatch replicated): its partial output
+    against the oracle's partial output of the same share."""
+    S = W.tp_share(W.make_layer(SMALL[base], 0), P, r)
+    ref = oracle.layer(S, want_intermediates=True)
+    layer, out = run_layer(S)
+    check_layer(S, ref, layer, out)
+
+
+@pytest.mark.parametrize("P", [2, 4, 16])
+def test_ep_share_ffn(P):
+    """Each rank's expert-parallel share: the grouped FFN over its block of
+    united experts alone (offsets and weights from the block's first expert
+    on) against the oracle on those rows, and no other row written; with 16
+    ranks over 15 united experts one rank has none."""
+    L, ref = case("fine-s", 0)
+    cfg = L.cfg
+    cap = cfg.T * cfg.top_k
+    w = device_weights(L)
+    a = torch.full((cap, cfg.d), 7.0, device="cuda", dtype=torch.bfloat16)
+    a[:ref["N"]] = dev_tensor(to_storage(ref["x_perm"], cfg.dtype), cfg.dtype)
+    offs = torch.from_numpy(ref["offsets"]).cuda()
+    sentinel = -3.0
+    for r in range(P):
+        g0, g1 = W.ep_groups(cfg.G, P, r)
+        if g0 == g1:
+            continue
+        lo, hi = int(ref["offsets"][g0]), int(ref["offsets"][g1])
+        y = torch.full_like(a, sentinel)
+        ys, hs = B.ffn(offs[g0:g1 + 1], a, w["w_gate"][g0:g1], w["w_up"][g0:g1], w["w_down"][g0:g1], y=y)
+        torch.cuda.synchronize()
+        assert_close_rows(host_f32(hs[lo:hi]), ref["h"][lo:hi], cfg.dtype, f"h rank {r}")
+        assert_close_rows(host_f32(ys[lo:hi]), ref["y"][lo:hi], cfg.dtype, f"y rank {r}")
+        assert bool((ys[:lo] == sentinel).all()) and bool((ys[hi:] == sentinel).all()), f"rank {r}"
+
+
 def full_case(name):
     cfg = W.CONFIGS[name]
     L = W.make_layer(cfg, 0)
@@ -501,9 +542,11 @@ def test_partial_brownout_layer(theta):
     check_layer(PL, ref, layer, out)
 
 
-@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral", "partial"])
+@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral", "partial", "mixtral-tp8"])
 def test_full_size_sampled(name):
-    L = full_case(name)
+    """Full-size workloads; mixtral-tp8 is rank 3's share of the Mixtral-shaped
+    layer under 8-way tensor parallelism (d_ff 1792)."""
+    L = W.tp_share(full_case("mixtral"), 8, 3) if name == "mixtral-tp8" else full_case(name)
     cfg = L.cfg
     layer, out = run_layer(L)
     # integer outputs in full
