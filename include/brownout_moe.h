@@ -154,6 +154,10 @@ BMOE_API bmoe_status brownout_moe_route(const bmoe_desc* desc, const void* x, co
  * [-1, G) count as -1). x [T,d] (dtype). counts [G], offsets [G+1],
  * perm_token [T*k], slot_row [T,k] int32; x_perm [T*k, d] (dtype). Rows at
  * and beyond N are left unspecified.
+ * x_perm NULL: the permutation only (counts, offsets, perm_token, slot_row);
+ * no row is copied and x is not read (it may be NULL). This is the first half
+ * of the fused path, whose FFN gathers its rows from x through perm_token
+ * (brownout_moe_ffn_gather).
  * workspace: bmoe_workspace_bytes(desc, BMOE_STAGE_DISPATCH) bytes, 256-byte
  * aligned, ALL ZERO before the first call that uses it; every call leaves it
  * all zero again when it completes on the stream. Two calls that share a
@@ -212,6 +216,29 @@ BMOE_API bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t
                                   int32_t d_ff, const int32_t* offsets, const void* h,
                                   const void* w_down, void* y, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/* Fused gather (the same FFN, Sec. 2.1, without the x_perm copy): the gate/up
+ * GEMM reads row r of its activations as a[a_rows[r], :] instead of a[r, :],
+ * straight from the token rows: with a = x [T, d], a_count = T and a_rows =
+ * the perm_token that brownout_moe_dispatch wrote (with x_perm NULL there),
+ * the results are bit-identical to dispatch's x_perm followed by
+ * brownout_moe_ffn. a_rows [rows_cap] int32 in DEVICE memory; entries are
+ * clamped into [0, a_count) (never read out of bounds); a [a_count, d]
+ * (dtype), 16-byte aligned; a_count * d * element size must stay below
+ * 2^32 bytes (BMOE_ERR_SHAPE otherwise). NULL a_rows with rows_cap > 0 is
+ * BMOE_ERR_NULL. Every other argument and rule as brownout_moe_ffn /
+ * brownout_moe_ffn_gate_up; the down GEMM is unchanged (h is already in row
+ * order). */
+BMOE_API bmoe_status brownout_moe_ffn_gather(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                    int32_t d_ff, const int32_t* offsets, const int32_t* a_rows,
+                                    int32_t a_count, const void* a, const void* w_gate, const void* w_up,
+                                    const void* w_down, void* h, void* y, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+BMOE_API bmoe_status brownout_moe_ffn_gate_up_gather(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                            int32_t d_ff, const int32_t* offsets, const int32_t* a_rows,
+                                            int32_t a_count, const void* a, const void* w_gate,
+                                            const void* w_up, void* h, void* workspace,
+                                            size_t workspace_bytes, void* stream);
 
 /*
  * brownout_moe_combine -- weighted sum back into token order (Sec. 2.1: the

@@ -27,7 +27,8 @@ STATUS = {0: "BMOE_OK", 1: "BMOE_ERR_NULL", 2: "BMOE_ERR_SHAPE", 3: "BMOE_ERR_AL
 
 EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_status_str",
             "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
-            "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine")
+            "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
+            "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather")
 
 
 class BmoeError(RuntimeError):
@@ -89,6 +90,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_ffn_gate_up.argtypes = [I32] * 5 + [P] * 6 + [SZ, P]
     lib.brownout_moe_ffn_gate_up.restype = I32
     lib.brownout_moe_ffn_down.argtypes = [I32] * 5 + [P] * 5 + [SZ, P]
+    lib.brownout_moe_ffn_gather.argtypes = [I32] * 5 + [P, P, I32] + [P] * 7 + [SZ, P]
+    lib.brownout_moe_ffn_gather.restype = I32
+    lib.brownout_moe_ffn_gate_up_gather.argtypes = [I32] * 5 + [P, P, I32] + [P] * 5 + [SZ, P]
+    lib.brownout_moe_ffn_gate_up_gather.restype = I32
     lib.brownout_moe_ffn_down.restype = I32
     lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
     lib.brownout_moe_combine.restype = I32
@@ -175,22 +180,27 @@ def route(desc: Desc, x: Optional[torch.Tensor], w_router: Optional[torch.Tensor
     return o
 
 
-def dispatch(desc: Desc, slot_group: torch.Tensor, x: torch.Tensor, workspace: torch.Tensor, *,
-             out: Optional[Dict[str, torch.Tensor]] = None, stream=None) -> Dict[str, torch.Tensor]:
+def dispatch(desc: Desc, slot_group: torch.Tensor, x: Optional[torch.Tensor], workspace: torch.Tensor, *,
+             out: Optional[Dict[str, torch.Tensor]] = None, copy_rows: bool = True,
+             stream=None) -> Dict[str, torch.Tensor]:
+    """copy_rows=False: the permutation only (no x_perm; x may be None), for
+    the FFN that gathers its rows itself (ffn_gather)."""
     T, k, G, d = desc.T, desc.top_k, desc.G, desc.d
-    dev = x.device
+    dev = slot_group.device
     _dev(slot_group, "slot_group", torch.int32, (T, k))
-    _dev(x, "x", desc.torch_dtype, (T, d))
+    if copy_rows or x is not None:
+        _dev(x, "x", desc.torch_dtype, (T, d))
     _dev(workspace, "workspace")
     o = dict(out) if out else {}
     o.setdefault("counts", _empty((G,), torch.int32, dev))
     o.setdefault("offsets", _empty((G + 1,), torch.int32, dev))
     o.setdefault("perm_token", _empty((max(T * k, 1),), torch.int32, dev))
     o.setdefault("slot_row", _empty((T, k), torch.int32, dev))
-    o.setdefault("x_perm", _empty((max(T * k, 1), d), desc.torch_dtype, dev))
+    if copy_rows:
+        o.setdefault("x_perm", _empty((max(T * k, 1), d), desc.torch_dtype, dev))
     st = load_library().brownout_moe_dispatch(
         ctypes.byref(desc), _p(slot_group), _p(x), _p(o["counts"]), _p(o["offsets"]),
-        _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]), _p(workspace),
+        _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]) if copy_rows else None, _p(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "brownout_moe_dispatch")
     return o
@@ -260,6 +270,50 @@ def ffn_gate_up(offsets, a, w_gate, w_up, *, h=None, workspace=None, stream=None
     return h
 
 
+def ffn_gather(offsets: torch.Tensor, a_rows: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor,
+               w_up: torch.Tensor, w_down: torch.Tensor, *, h=None, y=None, workspace=None, stream=None):
+    """ffn with the gate/up activations gathered: row r reads a[a_rows[r]]
+    (a_rows: the dispatch's perm_token, a: x). rows_cap = a_rows.numel().
+    Returns (y, h)."""
+    n_seg, d_ff, d = w_gate.shape
+    rows_cap, dt = a_rows.numel(), a.dtype
+    dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
+    _dev(a_rows, "a_rows", torch.int32, (rows_cap,))
+    _dev(a, "a", dt)
+    if a.dim() != 2 or a.shape[1] != d:
+        raise ValueError(f"a must be [rows, {d}]")
+    _dev(w_gate, "w_gate", dt, (n_seg, d_ff, d))
+    _dev(w_up, "w_up", dt, (n_seg, d_ff, d))
+    _dev(w_down, "w_down", dt, (n_seg, d, d_ff))
+    h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
+    y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, a.device)
+    wsp, wsn = _ws(workspace)
+    st = load_library().brownout_moe_ffn_gather(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a_rows),
+                                                a.shape[0], _p(a), _p(w_gate), _p(w_up), _p(w_down), _p(h),
+                                                _p(y), wsp, wsn, _stream(stream))
+    _check(st, "brownout_moe_ffn_gather")
+    return y, h
+
+
+def ffn_gate_up_gather(offsets, a_rows, a, w_gate, w_up, *, h=None, workspace=None, stream=None):
+    n_seg, d_ff, d = w_gate.shape
+    rows_cap, dt = a_rows.numel(), a.dtype
+    dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
+    _dev(a_rows, "a_rows", torch.int32, (rows_cap,))
+    _dev(a, "a", dt)
+    if a.dim() != 2 or a.shape[1] != d:
+        raise ValueError(f"a must be [rows, {d}]")
+    _dev(w_gate, "w_gate", dt, (n_seg, d_ff, d))
+    _dev(w_up, "w_up", dt, (n_seg, d_ff, d))
+    h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
+    wsp, wsn = _ws(workspace)
+    st = load_library().brownout_moe_ffn_gate_up_gather(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a_rows),
+                                                        a.shape[0], _p(a), _p(w_gate), _p(w_up), _p(h), wsp, wsn,
+                                                        _stream(stream))
+    _check(st, "brownout_moe_ffn_gate_up_gather")
+    return h
+
+
 def ffn_down(offsets, h, w_down, *, y=None, workspace=None, stream=None):
     n_seg, d, d_ff = w_down.shape
     rows_cap, dt = h.shape[0], h.dtype
@@ -305,11 +359,17 @@ class LayerForward:
     marshalled once; a call checks only x and looks up the current stream, so
     the host cost per call stays a few microseconds (decode-sized layers take
     less GPU time than the checks of the free functions).
+
+    fused_gather=True: dispatch writes only the permutation and the gate/up
+    GEMM gathers its rows from x (no x_perm buffer); ffn and ffn_gate_up then
+    take x. Results are bit-identical to the unfused path.
     """
 
-    def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True):
+    def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True,
+                 fused_gather: bool = False):
         self.desc = desc
         self.w = weights
+        self.fused_gather = fused_gather
         _check(validate(desc), "bmoe_validate")
         T, k, d, G, E = desc.T, desc.top_k, desc.d, desc.G, desc.E
         dt = desc.torch_dtype
@@ -321,12 +381,13 @@ class LayerForward:
             "dispatch": {"counts": _empty((G,), torch.int32, device),
                          "offsets": _empty((G + 1,), torch.int32, device),
                          "perm_token": _empty((rows,), torch.int32, device),
-                         "slot_row": _empty((T, k), torch.int32, device),
-                         "x_perm": _empty((rows, d), dt, device)},
+                         "slot_row": _empty((T, k), torch.int32, device)},
             "h": _empty((rows, desc.d_ff), dt, device),
             "y": _empty((rows, d), dt, device),
             "out": _empty((T, d), dt, device),
         }
+        if not fused_gather:
+            self.bufs["dispatch"]["x_perm"] = _empty((rows, d), dt, device)
         self.ws = new_dispatch_workspace(desc, device)
         self.ffn_ws = new_ffn_workspace(desc, device) if stream_k else None
         if desc.d_ff_shared:
@@ -356,15 +417,19 @@ class LayerForward:
         r, dp = b["route"], b["dispatch"]
         self._route_args = (ptr(w["w_router"]), ptr(w.get("bias")), None, ptr(w["e2g"]), ptr(r["topk_idx"]),
                             ptr(r["topk_w"]), ptr(r["slot_group"]), ptr(r["slot_gate"]), None)
+        fused = self.fused_gather
         self._dispatch_args = (ptr(dp["counts"]), ptr(dp["offsets"]), ptr(dp["perm_token"]), ptr(dp["slot_row"]),
-                               ptr(dp["x_perm"]), ptr(self.ws), self.ws.numel())
+                               None if fused else ptr(dp["x_perm"]), ptr(self.ws), self.ws.numel())
         rows = max(T * k, 1)
-        self._gate_up_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(dp["x_perm"]), ptr(w["w_gate"]),
+        # fused: (.., offsets, a_rows, a_count) then x's pointer at call time
+        a_src = (ptr(dp["perm_token"]), T) if fused else (ptr(dp["x_perm"]),)
+        self._gate_up_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), *a_src, ptr(w["w_gate"]),
                               ptr(w["w_up"]), ptr(b["h"]), wsp, wsn)
         self._down_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(b["h"]), ptr(w["w_down"]), ptr(b["y"]),
                            wsp, wsn)
-        self._ffn_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), ptr(dp["x_perm"]), ptr(w["w_gate"]),
+        self._ffn_args = (dtype, G, rows, d, f, ptr(dp["offsets"]), *a_src, ptr(w["w_gate"]),
                           ptr(w["w_up"]), ptr(w["w_down"]), ptr(b["h"]), ptr(b["y"]), wsp, wsn)
+        self._a_at = 8 if fused else None  # where x's pointer goes in the fused argument lists
         self._combine_args = (ptr(dp["slot_row"]), ptr(r["slot_gate"]), ptr(b["y"]),
                               ptr(b["y_sh"]) if desc.d_ff_shared else None, ptr(b["out"]))
         if desc.d_ff_shared:
@@ -396,12 +461,27 @@ class LayerForward:
                "brownout_moe_dispatch")
         return self.bufs["dispatch"]
 
-    def ffn(self, stream=None):
-        _check(self._lib.brownout_moe_ffn(*self._ffn_args, self._s(stream)), "brownout_moe_ffn")
+    def _fused_args(self, args, x):
+        if x is None:
+            raise ValueError("the fused-gather layer's FFN reads x: pass x")
+        i = self._a_at
+        return (*args[:i], self._x(x), *args[i:])
+
+    def ffn(self, stream=None, x=None):
+        if self.fused_gather:
+            _check(self._lib.brownout_moe_ffn_gather(*self._fused_args(self._ffn_args, x), self._s(stream)),
+                   "brownout_moe_ffn_gather")
+        else:
+            _check(self._lib.brownout_moe_ffn(*self._ffn_args, self._s(stream)), "brownout_moe_ffn")
         return self.bufs["y"], self.bufs["h"]
 
-    def ffn_gate_up(self, stream=None):
-        _check(self._lib.brownout_moe_ffn_gate_up(*self._gate_up_args, self._s(stream)), "brownout_moe_ffn_gate_up")
+    def ffn_gate_up(self, stream=None, x=None):
+        if self.fused_gather:
+            _check(self._lib.brownout_moe_ffn_gate_up_gather(*self._fused_args(self._gate_up_args, x),
+                                                             self._s(stream)), "brownout_moe_ffn_gate_up_gather")
+        else:
+            _check(self._lib.brownout_moe_ffn_gate_up(*self._gate_up_args, self._s(stream)),
+                   "brownout_moe_ffn_gate_up")
         return self.bufs["h"]
 
     def ffn_down(self, stream=None):
@@ -422,7 +502,7 @@ class LayerForward:
     def __call__(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         self.route(x, stream)
         self.dispatch(x, stream)
-        self.ffn(stream)
+        self.ffn(stream, x=x)
         if self.desc.d_ff_shared:
             self.shared(x, stream)
         return self.combine(stream)

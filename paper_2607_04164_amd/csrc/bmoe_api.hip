@@ -86,9 +86,10 @@ bmoe_status brownout_moe_dispatch(const bmoe_desc* d, const int32_t* slot_group,
     bmoe_status st = bmoe_validate(d);
     if (st != BMOE_OK) return st;
     if (d->T == 0) return BMOE_OK;
-    if (!slot_group || !x || !counts || !offsets || !perm_token || !slot_row || !x_perm)
+    // x_perm NULL: the permutation only (x is then not read and may be NULL)
+    if (!slot_group || !counts || !offsets || !perm_token || !slot_row || (x_perm && !x))
         return BMOE_ERR_NULL;
-    if (!aligned16(x) || !aligned16(x_perm)) return BMOE_ERR_ALIGN;
+    if (x_perm && (!aligned16(x) || !aligned16(x_perm))) return BMOE_ERR_ALIGN;
     if (!ws || ws_bytes < dispatch_ws_bytes(d->T, d->G)) return BMOE_ERR_WORKSPACE;
     if (((uintptr_t)ws & 255u) != 0) return BMOE_ERR_ALIGN;
     DispatchArgs a{slot_group, x, counts, offsets, perm_token, slot_row, x_perm, ws,
@@ -100,9 +101,12 @@ bmoe_status brownout_moe_dispatch(const bmoe_desc* d, const int32_t* slot_group,
 
 namespace {
 
+// a_rows != nullptr: the gate/up GEMM reads row r of its A operand from
+// a[a_rows[r]], a holding a_count rows
 bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
                        const int32_t* offsets, const void* a, const void* w_gate, const void* w_up,
-                       const void* w_down, void* h, void* y, void* ws, size_t ws_bytes, void* stream) {
+                       const void* w_down, void* h, void* y, void* ws, size_t ws_bytes, void* stream,
+                       const int32_t* a_rows = nullptr, int32_t a_count = 0) {
     if (dtype != BMOE_F32 && dtype != BMOE_BF16) return BMOE_ERR_UNSUPPORTED;
     if (n_seg < 1 || n_seg > BMOE_MAX_EXPERTS || rows_cap < 0) return BMOE_ERR_SHAPE;
     if (d < 8 || d % 8 != 0 || d_ff < 8 || d_ff % 8 != 0) return BMOE_ERR_SHAPE;
@@ -120,6 +124,12 @@ bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap,
     if (dtype != BMOE_BF16) ws = nullptr;  // the fp32 kernels take no workspace
     if (ws && ws_bytes < ffn_workspace_bytes()) return BMOE_ERR_WORKSPACE;
     FfnArgs args{offsets, a, w_gate, w_up, w_down, h, y, ws, ws_bytes, n_seg, rows_cap, d, d_ff, dtype};
+    if (a_rows) {
+        // the copy kernels address a gathered source with 32-bit byte offsets
+        if (a_count < 1 || (int64_t)a_count * d * elem_bytes(dtype) >= ((int64_t)1 << 32)) return BMOE_ERR_SHAPE;
+        args.a_rows = a_rows;
+        args.a_count = a_count;
+    }
     return hip_status(launch_ffn(args, (hipStream_t)stream, part));
 }
 
@@ -133,6 +143,24 @@ bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int
                              size_t workspace_bytes, void* stream) {
     return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, workspace,
                       workspace_bytes, stream);
+}
+
+bmoe_status brownout_moe_ffn_gather(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
+                                    const int32_t* offsets, const int32_t* a_rows, int32_t a_count,
+                                    const void* a, const void* w_gate, const void* w_up, const void* w_down,
+                                    void* h, void* y, void* workspace, size_t workspace_bytes, void* stream) {
+    if (rows_cap > 0 && !a_rows) return BMOE_ERR_NULL;
+    return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, workspace,
+                      workspace_bytes, stream, a_rows, a_count);
+}
+
+bmoe_status brownout_moe_ffn_gate_up_gather(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                            int32_t d_ff, const int32_t* offsets, const int32_t* a_rows,
+                                            int32_t a_count, const void* a, const void* w_gate, const void* w_up,
+                                            void* h, void* workspace, size_t workspace_bytes, void* stream) {
+    if (rows_cap > 0 && !a_rows) return BMOE_ERR_NULL;
+    return ffn_common(1, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, nullptr, h, nullptr,
+                      workspace, workspace_bytes, stream, a_rows, a_count);
 }
 
 bmoe_status brownout_moe_ffn_gate_up(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,

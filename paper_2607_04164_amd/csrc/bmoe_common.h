@@ -172,7 +172,18 @@ struct FfnArgs {
     void* ws;  // optional stream-K workspace (nullptr: one tile per workgroup)
     size_t ws_bytes;
     int n_seg, rows_cap, d, d_ff, dtype;
+    // gathered A operand of the gate/up GEMM: row r is a[a_rows[r]] (a has
+    // a_count rows); nullptr: row r is a[r]
+    const int32_t* a_rows = nullptr;
+    int a_count = 0;
 };
+
+// Row of the A operand that GEMM row r reads: a_rows[r] clamped into the
+// source, or r itself when the operand is not gathered.
+__device__ __forceinline__ int gathered_row(const int32_t* a_rows, int a_count, int r) {
+    if (!a_rows) return r;
+    return min(max(a_rows[r], 0), a_count - 1);
+}
 // bytes of the stream-K workspace on the current device
 size_t ffn_workspace_bytes();
 // part: 0 = both GEMMs, 1 = gate/up only, 2 = down only

@@ -230,6 +230,34 @@ __global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict_
     }
 }
 
+// The permutation without the row copies (for an FFN that gathers its rows
+// from x itself): one thread per slot writes its row and the row's token.
+__global__ __launch_bounds__(256) void permute_index_kernel(const int32_t* __restrict__ slot_group,
+                                                            int32_t* __restrict__ slot_row,
+                                                            const int32_t* __restrict__ offsets,
+                                                            int32_t* __restrict__ perm_token, void* ws, int T,
+                                                            int k, int G, int ntiles, int rows_cap) {
+    const int tid = threadIdx.x;
+    if (blockIdx.x == 0) {
+        // leave the look-back state all zero for the next call
+        DispatchWs* hdr = (DispatchWs*)ws;
+        uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
+        const int n = ntiles * G;
+        for (int i = tid; i < n; i += 256) status[i] = 0ull;
+        if (tid == 0) hdr->ticket = 0;
+    }
+    const int64_t o = (int64_t)blockIdx.x * 256 + tid;
+    if (o >= (int64_t)T * k) return;
+    const int g = slot_group[o];
+    int row = -1;
+    if (g >= 0 && g < G) {
+        row = offsets[g] + slot_row[o];
+        if (row < 0 || row >= rows_cap) row = -1;
+        else perm_token[row] = (int)(o / k);
+    }
+    slot_row[o] = row;
+}
+
 }  // namespace
 
 size_t dispatch_ws_bytes(int T, int G) {
@@ -244,6 +272,13 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
                        a.counts, a.offsets, a.ws, a.T, a.k, a.G, ntiles);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (a.x_perm == nullptr) {
+        const int64_t slots = (int64_t)a.T * a.k;
+        hipLaunchKernelGGL(permute_index_kernel, dim3((unsigned)((slots + 255) / 256)), dim3(256), 0, s,
+                           a.slot_group, a.slot_row, a.offsets, a.perm_token, a.ws, a.T, a.k, a.G, ntiles,
+                           a.T * a.k);
+        return hipGetLastError();
+    }
     const int nch = a.d * a.elem_bytes / 16;
     hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
                        a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,

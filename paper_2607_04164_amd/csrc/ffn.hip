@@ -36,6 +36,8 @@ struct GemmParams {
     const int32_t* offsets;
     int n_seg, rows_cap, N, K;
     int sk_min_idle;  // stream-K split threshold (average idle K-steps per workgroup)
+    const int32_t* a_rows = nullptr;  // gathered A: row r is A[a_rows[r]] (A has a_count rows)
+    int a_count = 0;
 };
 
 template <bool GATED, int BM, int BN, int BK>
@@ -64,17 +66,17 @@ __device__ __forceinline__ int xcd_swizzle(int b, int nblocks) {
     return (b & 7) * per + (b >> 3);
 }
 
+// arow[i]: source row of this thread's A chunk i (see gemm_arows)
 template <class C>
 __device__ __forceinline__ void gemm_gload(uint4 (&ra)[C::A_CH], uint4 (&rb)[C::NMAT][C::B_CH],
-                                           const uint16_t* A, const uint16_t* B0, const uint16_t* B1,
-                                           int tid, int k0, int m0, int m_end, int n0, int N, int K) {
+                                           const uint16_t* A, const int (&arow)[C::A_CH], const uint16_t* B0,
+                                           const uint16_t* B1, int tid, int k0, int n0, int N, int K) {
 #pragma unroll
     for (int i = 0; i < C::A_CH; ++i) {
         const int c = tid + kGemmThreads * i;
-        const int r = c / C::KCH, cc = c % C::KCH;
-        const int gm = min(m0 + r, m_end - 1);
+        const int cc = c % C::KCH;
         const int gk = k0 + cc * 8;
-        ra[i] = gk < K ? *(const uint4*)(A + (size_t)gm * K + gk) : make_uint4(0, 0, 0, 0);
+        ra[i] = gk < K ? *(const uint4*)(A + (size_t)arow[i] * K + gk) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int mat = 0; mat < C::NMAT; ++mat) {
@@ -87,6 +89,17 @@ __device__ __forceinline__ void gemm_gload(uint4 (&ra)[C::A_CH], uint4 (&rb)[C::
             const int gk = k0 + cc * 8;
             rb[mat][i] = gk < K ? *(const uint4*)(B + (size_t)gn * K + gk) : make_uint4(0, 0, 0, 0);
         }
+    }
+}
+
+// source rows of this thread's A chunks for the tile's rows [m0, m_end)
+// (clamped to the last row; gathered through a_rows when the operand is)
+template <class C>
+__device__ __forceinline__ void gemm_arows(int (&arow)[C::A_CH], const GemmParams& p, int tid, int m0, int m_end) {
+#pragma unroll
+    for (int i = 0; i < C::A_CH; ++i) {
+        const int c = tid + kGemmThreads * i;
+        arow[i] = gathered_row(p.a_rows, p.a_count, min(m0 + c / C::KCH, m_end - 1));
     }
 }
 
@@ -198,13 +211,15 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_kernel(GemmParam
     const int l32 = lane & 31, hi8 = (lane >> 5) * 8;
     const int nk = ceil_div(K, BK);
 
-    gemm_gload<C>(ra, rb, p.A, Bm[0], Bm[1], tid, 0, m0, m_end, n0, N, K);
+    int arow[C::A_CH];
+    gemm_arows<C>(arow, p, tid, m0, m_end);
+    gemm_gload<C>(ra, rb, p.A, arow, Bm[0], Bm[1], tid, 0, n0, N, K);
     gemm_sstore<C>(ra, rb, sA, sB, tid, 0);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
         const bool more = kt + 1 < nk;
-        if (more) gemm_gload<C>(ra, rb, p.A, Bm[0], Bm[1], tid, (kt + 1) * BK, m0, m_end, n0, N, K);
+        if (more) gemm_gload<C>(ra, rb, p.A, arow, Bm[0], Bm[1], tid, (kt + 1) * BK, n0, N, K);
         const uint16_t* a_base = sA + (size_t)(buf * BM + wm * C::WTM + l32) * C::LROW + hi8;
         const uint16_t* b_base = sB + (size_t)(buf * BN + wn * C::WTN + l32) * C::LROW + hi8;
         if constexpr (FDB) {
@@ -525,12 +540,15 @@ __device__ __forceinline__ void dma_sources(DmaSrc<C>& src, const GemmParams& p,
                                             int lane) {
     const int K = p.K, N = p.N;
     const int lrow = lane / C::KC, lchk = lane % C::KC;
-    src.a_base = (const char*)(p.A + (size_t)tc.m0 * K);
+    // offsets from the tile's first row, or from row 0 of the source when the
+    // rows are gathered (the host keeps a_count * K * 2 below 2^32)
+    const int base_row = p.a_rows ? 0 : tc.m0;
+    src.a_base = (const char*)(p.A + (size_t)base_row * K);
 #pragma unroll
     for (int i = 0; i < C::A_DMA; ++i) {
         const int r = (wave * C::A_DMA + i) * C::ROWS_PER_DMA + lrow;
-        const int row = min(tc.m0 + r, tc.m_end - 1);
-        src.a_off[i] = (uint32_t)(((row - tc.m0) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
+        const int row = gathered_row(p.a_rows, p.a_count, min(tc.m0 + r, tc.m_end - 1));
+        src.a_off[i] = (uint32_t)(((size_t)(row - base_row) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
     // a wave's B rows lie in one matrix (gate or up for the gated GEMM)
     static_assert(!GATED || (C::B_DMA * C::ROWS_PER_DMA * 2 == C::BN), "B rows of a wave in one matrix");
@@ -862,13 +880,14 @@ __global__ __launch_bounds__(256) void ffn_f32_gateup_kernel(const float* __rest
                                                              const float* __restrict__ wu,
                                                              float* __restrict__ h,
                                                              const int32_t* __restrict__ offsets,
-                                                             int n_seg, int rows_cap, int d, int d_ff) {
+                                                             int n_seg, int rows_cap, int d, int d_ff,
+                                                             const int32_t* __restrict__ a_rows, int a_count) {
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (idx >= (int64_t)rows_cap * d_ff) return;
     const int row = (int)(idx / d_ff), j = (int)(idx % d_ff);
     const int s = find_segment(offsets, n_seg, rows_cap, row);
     if (s < 0) return;
-    const float* ar = a + (size_t)row * d;
+    const float* ar = a + (size_t)gathered_row(a_rows, a_count, row) * d;
     const float* gr = wg + ((size_t)s * d_ff + j) * d;
     const float* ur = wu + ((size_t)s * d_ff + j) * d;
     float g = 0.f, u = 0.f;
@@ -929,7 +948,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
         if (up) {
             hipLaunchKernelGGL(ffn_f32_gateup_kernel, dim3((unsigned)ceil_div64(n1, 256)), dim3(256), 0, s,
                                (const float*)a.a, (const float*)a.w_gate, (const float*)a.w_up, (float*)a.h,
-                               a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff);
+                               a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff, a.a_rows, a.a_count);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
@@ -946,6 +965,8 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (up) {
         GemmParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up,
                       (uint16_t*)a.h, a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
+        g1.a_rows = a.a_rows;
+        g1.a_count = a.a_count;
         hipError_t e = tile == kTileDma   ? launch_gemm_dma<true>(g1, a.ws, a.ws_bytes, s)
                        : tile == kTile256 ? launch_gemm<true, 256, 128, 64, kFdb256>(g1, s)
                                           : launch_gemm<true, 128, 128, 64, true>(g1, s);

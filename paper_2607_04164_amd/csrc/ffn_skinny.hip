@@ -40,28 +40,30 @@ struct SkinnyParams {
     uint16_t* C;         // [rows_cap, N]
     const int32_t* offsets;
     int n_seg, rows_cap, N, K;
+    const int32_t* a_rows = nullptr;  // gathered A: row r is A[a_rows[r]] (A has a_count rows)
+    int a_count = 0;
 };
 
 // LDS byte offset of logical 16-byte chunk c of activation row r
 __device__ __forceinline__ int sk_off(int r, int c) { return r * kSkRowBytes + ((c ^ (r & 15)) << 4); }
 
-// Chunk c of the pass's activation rows [m0, m0+64) (clamped to the segment)
+// Chunk c of the pass's activation rows (source rows xrow, see the kernel)
 // into xs, and of the lane's weight rows into wv. Addresses past the end of a
 // row or past the last chunk are clamped to column 0 (finite values); the
 // activations of those columns are zeroed when they are written to LDS, so
 // their products vanish and no load result is touched before it is used.
 template <int NMAT>
 __device__ __forceinline__ void sk_load(const SkinnyParams& p, const uint16_t* const (&wp)[NMAT], int c, int nch,
-                                        int m0, int end, int q, v4u (&xs)[kSkXLoads], v4u (&wv)[NMAT][8]) {
+                                        const int (&xrow)[kSkXLoads], int q, v4u (&xs)[kSkXLoads],
+                                        v4u (&wv)[NMAT][8]) {
     const int K = p.K;
     const int kc0 = min(c, nch - 1) * kSkKC;
 #pragma unroll
     for (int j = 0; j < kSkXLoads; ++j) {
         const int i = threadIdx.x + kSkThreads * j;
-        const int row = min(m0 + (i >> 5), end - 1);
         int col = kc0 + (i & 31) * 8;
         if (col >= K) col = 0;
-        xs[j] = *(const v4u*)(p.A + (size_t)row * K + col);
+        xs[j] = *(const v4u*)(p.A + (size_t)xrow[j] * K + col);
     }
     // the activations are issued before the weights: their LDS store (one
     // chunk earlier than the weights' MFMAs) then waits only for older loads
@@ -134,20 +136,26 @@ __global__ __launch_bounds__(kSkThreads, 1) void skinny_gemm_kernel(SkinnyParams
         // two stages: chunk c's weights are loaded two chunks ahead, its
         // activations one chunk before they are written to LDS (a third stage
         // measured slower)
+        // source rows of this thread's activation loads: the pass's rows
+        // [m0, m0+64) clamped to the segment, gathered when A is
+        int xrow[kSkXLoads];
+#pragma unroll
+        for (int j = 0; j < kSkXLoads; ++j)
+            xrow[j] = gathered_row(p.a_rows, p.a_count, min(m0 + ((tid + kSkThreads * j) >> 5), end - 1));
         v4u xs0[kSkXLoads], xs1[kSkXLoads];
         v4u w0[NMAT][8], w1[NMAT][8];
-        sk_load<NMAT>(p, wp, 0, nch, m0, end, q, xs0, w0);
-        sk_load<NMAT>(p, wp, 1, nch, m0, end, q, xs1, w1);
+        sk_load<NMAT>(p, wp, 0, nch, xrow, q, xs0, w0);
+        sk_load<NMAT>(p, wp, 1, nch, xrow, q, xs1, w1);
         sk_store_x(xs0, slot0, 0, nch, K);
         __syncthreads();
         for (int c = 0; c < nch; c += 2) {
             sk_compute<NMAT>(acc, slot0, w0, r16, q);  // chunk c
             sk_store_x(xs1, slot1, c + 1, nch, K);     // chunk c+1 (slot released by the last barrier)
-            sk_load<NMAT>(p, wp, c + 2, nch, m0, end, q, xs0, w0);
+            sk_load<NMAT>(p, wp, c + 2, nch, xrow, q, xs0, w0);
             __syncthreads();
             sk_compute<NMAT>(acc, slot1, w1, r16, q);  // chunk c+1 (zero activations past the end)
             sk_store_x(xs0, slot0, c + 2, nch, K);     // chunk c+2
-            sk_load<NMAT>(p, wp, c + 3, nch, m0, end, q, xs1, w1);
+            sk_load<NMAT>(p, wp, c + 3, nch, xrow, q, xs1, w1);
             __syncthreads();
         }
 
@@ -198,6 +206,8 @@ hipError_t launch_ffn_skinny(const FfnArgs& a, hipStream_t s, int part) {
     if (up) {
         SkinnyParams g1{(const uint16_t*)a.a, (const uint16_t*)a.w_gate, (const uint16_t*)a.w_up, (uint16_t*)a.h,
                         a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
+        g1.a_rows = a.a_rows;
+        g1.a_count = a.a_count;
         hipError_t e = launch_skinny<true>(g1, s);
         if (e != hipSuccess) return e;
     }

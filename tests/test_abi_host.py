@@ -106,6 +106,10 @@ def test_entry_points_reject_before_launch(lib):
     assert lib.brownout_moe_dispatch(bd, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                      ctypes.c_void_p(0x10010), need, z) == ALIGN
     assert lib.brownout_moe_dispatch(bd, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == NULL
+    # dispatch without row copies (x_perm NULL): x may be NULL; with x_perm, x may not
+    assert lib.brownout_moe_dispatch(bd, FAKE, z, FAKE, FAKE, FAKE, FAKE, z, z, need, z) == WS
+    assert lib.brownout_moe_dispatch(bd, FAKE, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == NULL
+    assert lib.brownout_moe_dispatch(bd, FAKE, z, z, FAKE, FAKE, FAKE, z, FAKE, need, z) == NULL
     # ffn (and its halves)
     ffn = lib.brownout_moe_ffn
     assert ffn(9, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == UNSUP
@@ -119,6 +123,16 @@ def test_entry_points_reject_before_launch(lib):
                z) == ALIGN
     assert lib.brownout_moe_ffn_gate_up(1, 4, 128, 256, 512, FAKE, z, FAKE, FAKE, FAKE, z, 0, z) == NULL
     assert lib.brownout_moe_ffn_down(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, MISALIGNED, z, 0, z) == ALIGN
+    # fused gather: row indices required, the source small enough for 32-bit offsets
+    g = lib.brownout_moe_ffn_gather
+    assert g(1, 4, 128, 256, 512, FAKE, z, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == NULL
+    assert g(1, 4, 128, 256, 512, FAKE, FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    assert g(1, 4, 128, 4096, 512, FAKE, FAKE, 1 << 19, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    assert g(1, 4, 128, 256, 512, FAKE, FAKE, 64, MISALIGNED, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == ALIGN
+    assert g(1, 0, 128, 256, 512, FAKE, FAKE, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == SHAPE
+    gu = lib.brownout_moe_ffn_gate_up_gather
+    assert gu(1, 4, 128, 256, 512, FAKE, z, 64, FAKE, FAKE, FAKE, FAKE, z, 0, z) == NULL
+    assert gu(1, 4, 128, 256, 512, FAKE, FAKE, 64, FAKE, FAKE, z, FAKE, z, 0, z) == NULL
     # combine
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, z, z, z) == NULL
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
@@ -132,6 +146,7 @@ def test_zero_tokens_needs_no_pointers(lib):
     assert lib.brownout_moe_dispatch(bd, z, z, z, z, z, z, z, z, 0, z) == OK
     assert lib.brownout_moe_combine(bd, z, z, z, z, z, z) == OK
     assert lib.brownout_moe_ffn(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z, 0, z) == OK
+    assert lib.brownout_moe_ffn_gather(1, 4, 0, 256, 512, z, z, 0, z, z, z, z, z, z, z, 0, z) == OK
 
 
 def test_binding_refuses_host_tensors():

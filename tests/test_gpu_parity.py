@@ -484,6 +484,67 @@ def partial_layer(L):
 
 
 # ---------------------------------------------------------------------------
+# fused gather: the FFN reads its rows from x through perm_token
+
+GATHER = {
+    "tiny": SMALL["tiny"],                     # fp32 kernels
+    "mixtral-s": SMALL["mixtral-s"],           # 128-row register-staged tiles
+    "decode": SMALL["decode"],                 # skinny weight-streaming kernels
+    "dma": W.LayerConfig("dma", T=2100, d=256, E=8, top_k=2, G=4, d_ff=384, dtype="bf16", zipf_s=0.5),
+}
+
+
+@pytest.mark.parametrize("name", list(GATHER))
+@pytest.mark.parametrize("stream_k", [False, True], ids=["tiles", "stream_k"])
+def test_ffn_gather_bit_identical(name, stream_k):
+    """Dispatch without row copies + the gathering FFN writes the same bits as
+    dispatch's x_perm + the FFN, on every kernel path; the permutation-only
+    dispatch writes the same integers and leaves its workspace reusable."""
+    cfg = GATHER[name]
+    L = W.make_layer(cfg, 3)
+    ref = oracle.route(L.f32("x"), L.f32("w_router"), L.bias, L.e2g, cfg.top_k, cfg.norm_topk)
+    desc = desc_of(cfg)
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    sg = torch.from_numpy(ref["slot_group"]).cuda()
+    ws = B.new_dispatch_workspace(desc, "cuda")
+    full = B.dispatch(desc, sg, x, ws)
+    idx = B.dispatch(desc, sg, None, ws, copy_rows=False)
+    idx2 = B.dispatch(desc, sg, x, ws, copy_rows=False)  # workspace left zero by the previous call
+    torch.cuda.synchronize()
+    N = int(full["offsets"][-1].item())
+    for k in ("counts", "offsets", "slot_row"):
+        assert torch.equal(idx[k], full[k]) and torch.equal(idx2[k], full[k]), k
+    assert torch.equal(idx["perm_token"][:N], full["perm_token"][:N])
+    assert "x_perm" not in idx
+    fws = B.new_ffn_workspace(desc, "cuda") if stream_k else None
+    y0, h0 = B.ffn(full["offsets"], full["x_perm"], w["w_gate"], w["w_up"], w["w_down"], workspace=fws)
+    y1, h1 = B.ffn_gather(idx["offsets"], idx["perm_token"], x, w["w_gate"], w["w_up"], w["w_down"],
+                          workspace=fws)
+    h2 = B.ffn_gate_up_gather(idx["offsets"], idx["perm_token"], x, w["w_gate"], w["w_up"], workspace=fws)
+    torch.cuda.synchronize()
+    assert torch.equal(h1[:N], h0[:N]) and torch.equal(y1[:N], y0[:N])
+    assert torch.equal(h2[:N], h0[:N])
+
+
+@pytest.mark.parametrize("name", ["fine-s", "heavy-s", "tail"])
+def test_layer_fused_gather(name):
+    """The fused-gather layer: bit-identical to the four-call layer, and
+    within tolerance of the oracle."""
+    L, ref = case(name, 0)
+    cfg = L.cfg
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    out0 = B.LayerForward(desc_of(cfg), w)(x).clone()
+    layer = B.LayerForward(desc_of(cfg), w, fused_gather=True)
+    out1 = layer(x)
+    torch.cuda.synchronize()
+    assert "x_perm" not in layer.bufs["dispatch"]
+    assert torch.equal(out1, out0)
+    check_layer(L, ref, layer, out1)
+
+
+# ---------------------------------------------------------------------------
 # one GPU's share of a layer sharded over several GPUs
 
 @pytest.mark.parametrize("base,P,r", [("mixtral-s", 8, 0), ("mixtral-s", 8, 7), ("heavy-s", 4, 2)])
