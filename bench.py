@@ -38,8 +38,8 @@ VALU_F32_PEAK_TFLOPS = 157.3
 # --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
 # all of them). Valid only for the kernel sources they were taken with.
 TRAFFIC_RECORDS = {
-    "mixtral": {"src_sha1": "2639d3c2ef0b9ab731fbdf4c4e10549997f0d714",
-                "fetch_kib": 1732595.4, "write_kib": 312072.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "mixtral": {"src_sha1": "64f328a29101017f5a730dbde1b03d02163e754d",
+                "fetch_kib": 1765075.8, "write_kib": 291688.0, "fetch_scale": 2.0, "write_scale": 1.0,
                 "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
 }
 TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
@@ -278,8 +278,9 @@ def time_layer(cfg, args, dev):
     # read pass over 1 GiB evicts L2 and the 256 MB MALL (a read, so no dirty
     # lines are left to be written back inside the timed launch)
     cold_ms = {}
-    flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
-    flush.fill_(1)
+    # float32, so that sum() is one reduction over the buffer (an integer sum
+    # would first widen the whole buffer to int64, a 2 GiB write)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
     for s in stages:
         if s.startswith("ffn") or s == "shared_ffn":
             continue
