@@ -91,6 +91,10 @@ def parse():
     ap.add_argument("--fused-gather", action="store_true",
                     help="time the fused-gather path as the headline: dispatch writes only the permutation and "
                          "the gate/up GEMM gathers its rows from x (no x_perm copy)")
+    ap.add_argument("--distill", action="store_true",
+                    help="instead of the layer forward: time the evaluation of one candidate grouping of the "
+                         "workload's layer (parameter-average united experts, their FFN on the T tokens as "
+                         "calibration set, the routing-weighted distillation errors)")
     ap.add_argument("--no-compare-fused", action="store_true",
                     help="skip the second timing of the same layer on the fused-gather path")
     ap.add_argument("--theta", type=float, default=None,
@@ -319,6 +323,12 @@ def main():
     from paper_2607_04164_amd import binding as B
     from paper_2607_04164_amd import workload as W
 
+    if args.distill:
+        torch.cuda.set_device(0)
+        B.load_library()
+        bench_distill(args, torch.device("cuda:0"))
+        return
+
     if args.copy_probe_mib > 0:
         torch.cuda.set_device(0)
         copy_probe(args.copy_probe_mib)
@@ -454,6 +464,104 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(L, cfg0, share, args.share_rank, args.cpu_seconds)
 
+    print(json.dumps(result), flush=True)
+
+
+def bench_distill(args, dev):
+    """One candidate grouping of the search (Sec. 4.2), evaluated on the GPU:
+    the united experts start as their members' parameter average, run on the
+    T calibration tokens, and the errors of Eq. 5-6 follow. The members'
+    outputs are computed once (the calibration run records them) and are not
+    part of the timed step."""
+    import torch
+    from paper_2607_04164_amd import binding as B
+    from paper_2607_04164_amd import workload as W
+
+    cfg = W.CONFIGS[args.config]
+    if cfg.dtype != "bf16":
+        raise SystemExit("--distill runs the bf16 workloads")
+    T, d, E, G, f = cfg.T, cfg.d, cfg.E, cfg.G, cfg.d_ff
+    print(f"[bench] distill: generating {cfg.name} experts", file=sys.stderr, flush=True)
+    L = W.make_layer(cfg, args.seed, with_weights=False)
+    parts = [W.expert_weights(L, e) for e in range(E)]
+    to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    we = [to_dev(np.stack([p[j] for p in parts])) for j in range(3)]
+    del parts
+    x = to_dev(L.x)
+    e2g = torch.from_numpy(L.e2g).to(dev)
+    wfreq = torch.from_numpy(W.zipf_freq(L).astype(np.float32)).to(dev)
+    fws = B.new_ffn_workspace(B.make_desc(T, d, E, cfg.top_k, G, f, 0, 0, "bf16"), dev)
+    y_e = B.ffn_all_tokens(x, *we, workspace=fws)  # once per calibration run
+    wu = B.united_init(e2g, G, *we)
+    offs, a_rows = B.all_tokens_rows(G, T, dev)
+    h = torch.empty((G * T, f), dtype=torch.bfloat16, device=dev)
+    y_u = torch.empty((G * T, d), dtype=torch.bfloat16, device=dev)
+    dws = torch.empty(B.DISTILL_WS_BYTES, dtype=torch.uint8, device=dev)
+    mse = torch.zeros(G, dtype=torch.float64, device=dev)
+    tot = torch.zeros((), dtype=torch.float64, device=dev)
+    stages = {
+        "united_init": lambda: B.united_init(e2g, G, *we, out=wu),
+        "united_ffn": lambda: B.ffn_gather(offs, a_rows, x, *wu, h=h, y=y_u, workspace=fws),
+        "distill_mse": lambda: B.distill_mse(e2g, wfreq, y_e, y_u, T, workspace=dws, out=(mse, tot)),
+    }
+
+    def step():
+        for fn in stages.values():
+            fn()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    s = 2
+    work = {"united_init": ("hbm", 3 * (E + G) * d * f * s), "united_ffn": ("mfma", 6.0 * G * T * d * f),
+            "distill_mse": ("hbm", (E + G) * T * d * s)}
+    out = {}
+    for name, fn in stages.items():
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 3 if name == "united_ffn" else 10
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        sms = e0.elapsed_time(e1) / reps
+        kind, amt = work[name]
+        if kind == "hbm":
+            rate = amt / (sms * 1e-3) / 1e9
+            out[name] = {"us": round(sms * 1e3, 2), "bytes": int(amt), "GB_s": round(rate, 1),
+                         "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+        else:
+            rate = amt / (sms * 1e-3) / 1e12
+            out[name] = {"us": round(sms * 1e3, 2), "flop": amt, "TFLOP_s": round(rate, 1),
+                         "frac_of_peak": round(rate / MFMA_BF16_PEAK_TFLOPS, 4)}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    B.ffn_all_tokens(x, *we, workspace=fws)
+    e1.record()
+    torch.cuda.synchronize()
+    mse_h = mse.cpu().numpy().tolist()
+    dom = out["united_ffn"]
+    result = {
+        "metric": "grouping candidates evaluated per second (united init + united-expert FFN on the "
+                  "calibration tokens + routing-weighted distillation errors), 1 MI355X",
+        "value": round(1e3 / ms, 2), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded expert weights and tokens)",
+        "config": {"workload": f"grouping search on the {cfg.name} layer: E={E} experts, G={G} united, d={d}, "
+                               f"d_ff={f}, T={T} calibration tokens, zero distillation steps",
+                   "E": E, "G": G, "d": d, "d_ff": f, "T": T},
+        "roofline": {"kernel": "grouped_gemm_dma_kernel<gated> + <down> (united-expert FFN, gathered rows)",
+                     "bound": "mfma", "achieved": dom["TFLOP_s"], "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": dom["frac_of_peak"], "traffic": None},
+        "stages": out,
+        "expert_outputs_once_us": round(e0.elapsed_time(e1) * 1e3, 1),
+        "mse": [round(v, 6) for v in mse_h], "mse_total": round(float(tot.item()), 6),
+    }
     print(json.dumps(result), flush=True)
 
 

@@ -241,6 +241,48 @@ BMOE_API bmoe_status brownout_moe_ffn_gate_up_gather(int32_t dtype, int32_t n_se
                                             size_t workspace_bytes, void* stream);
 
 /*
+ * Grouping search (Sec. 4.2): what a candidate map costs in distillation
+ * error. The member experts' outputs f_e(x) and the united experts' outputs
+ * f_u(x) on the calibration tokens come from brownout_moe_ffn_gather with one
+ * segment per expert (rows e*T .. e*T+T-1 read token t = row mod T).
+ *
+ * brownout_moe_united_init -- the united experts' starting point: each united
+ * matrix is the element-wise average of its members' matrices (the parameter
+ * average the paper starts distillation from, Sec. 4.2 after Eq. 5).
+ *   w_*_u[r] = (sum over e with e2g[e] == r, ascending e, of w_*_e[e]) / count
+ * e2g [E] int32 in DEVICE memory (entries outside [0, G) belong to no group);
+ * w_gate_e, w_up_e [E, d_ff, d], w_down_e [E, d, d_ff]; w_gate_u, w_up_u
+ * [G, d_ff, d], w_down_u [G, d, d_ff] (dtype; bf16: fp32 sum, rounded once;
+ * f32: fp64 sum). An empty group gets zeros. E, G in 1..256.
+ */
+BMOE_API bmoe_status brownout_moe_united_init(int32_t dtype, int32_t E, int32_t G, int32_t d, int32_t d_ff,
+                                     const int32_t* e2g, const void* w_gate_e, const void* w_up_e,
+                                     const void* w_down_e, void* w_gate_u, void* w_up_u, void* w_down_u,
+                                     void* stream);
+
+/*
+ * brownout_moe_distill_mse -- distillation error of every group and the
+ * layer total (Eq. 5, Eq. 3 and Eq. 6):
+ *   alpha_e  = w_e / (sum of w over e's group)  (equal weights if that sum is 0)
+ *   t_r(x_t) = sum over the members e of r of alpha_e y_expert[e*T + t, :]
+ *   mse[r]   = mean over t < T and j < d of (y_united[r*T + t, j] - t_r(x_t)[j])^2
+ *   *mse_total = sum over r of beta_r mse[r],  beta_r = sum of w over r's members
+ * (the reward of the grouping search is -*mse_total). An empty group has
+ * mse 0 and beta 0. e2g [E] int32 and w_freq [E] float (routing frequencies)
+ * in DEVICE memory; y_expert [E*T, d], y_united [G*T, d] (dtype, 16-byte
+ * aligned); mse [G] double, mse_total (nullable) double, in DEVICE memory.
+ * Targets in fp32, squares accumulated in fp64 in a fixed order: results are
+ * deterministic. workspace: at least BMOE_DISTILL_WS_BYTES bytes of device
+ * memory, 8-byte aligned, contents need no initialisation (calls that can
+ * overlap must not share one). T == 0 writes nothing.
+ */
+#define BMOE_DISTILL_WS_BYTES 32768
+BMOE_API bmoe_status brownout_moe_distill_mse(int32_t dtype, int32_t E, int32_t G, int32_t T, int32_t d,
+                                     const int32_t* e2g, const float* w_freq, const void* y_expert,
+                                     const void* y_united, double* mse, double* mse_total, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/*
  * brownout_moe_combine -- weighted sum back into token order (Sec. 2.1: the
  * layer output is the gate-weighted sum of the expert outputs).
  *   out[t,:] = sum over i ascending with slot_row[t,i] >= 0 of

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Dict, Optional
+from typing import Dict, Optional, Tuple
 
 import torch
 
@@ -28,7 +28,9 @@ STATUS = {0: "BMOE_OK", 1: "BMOE_ERR_NULL", 2: "BMOE_ERR_SHAPE", 3: "BMOE_ERR_AL
 EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_status_str",
             "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
             "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
-            "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather")
+            "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather", "brownout_moe_united_init",
+            "brownout_moe_distill_mse")
+DISTILL_WS_BYTES = 32768
 
 
 class BmoeError(RuntimeError):
@@ -94,6 +96,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_ffn_gather.restype = I32
     lib.brownout_moe_ffn_gate_up_gather.argtypes = [I32] * 5 + [P, P, I32] + [P] * 5 + [SZ, P]
     lib.brownout_moe_ffn_gate_up_gather.restype = I32
+    lib.brownout_moe_united_init.argtypes = [I32] * 5 + [P] * 8
+    lib.brownout_moe_united_init.restype = I32
+    lib.brownout_moe_distill_mse.argtypes = [I32] * 5 + [P] * 7 + [SZ, P]
+    lib.brownout_moe_distill_mse.restype = I32
     lib.brownout_moe_ffn_down.restype = I32
     lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
     lib.brownout_moe_combine.restype = I32
@@ -312,6 +318,69 @@ def ffn_gate_up_gather(offsets, a_rows, a, w_gate, w_up, *, h=None, workspace=No
                                                         _stream(stream))
     _check(st, "brownout_moe_ffn_gate_up_gather")
     return h
+
+
+# ---------------------------------------------------------------------------
+# grouping search: expert outputs on calibration tokens, united init, errors
+
+def all_tokens_rows(n: int, T: int, device) -> Tuple[torch.Tensor, torch.Tensor]:
+    """(offsets, a_rows) that run n FFNs over the same T tokens with
+    ffn_gather: segment s covers rows s*T .. s*T+T-1, row r reads token r mod T."""
+    offsets = torch.arange(n + 1, dtype=torch.int32, device=device) * T
+    a_rows = torch.arange(T, dtype=torch.int32, device=device).repeat(n)
+    return offsets, a_rows
+
+
+def ffn_all_tokens(x: torch.Tensor, w_gate, w_up, w_down, *, workspace=None, stream=None) -> torch.Tensor:
+    """Every FFN of the stack on every token: [n*T, d], rows s*T + t = FFN_s(x_t)."""
+    n, T = w_gate.shape[0], x.shape[0]
+    offsets, a_rows = all_tokens_rows(n, T, x.device)
+    y, _ = ffn_gather(offsets, a_rows, x, w_gate, w_up, w_down, workspace=workspace, stream=stream)
+    return y
+
+
+def united_init(e2g: torch.Tensor, G: int, w_gate_e, w_up_e, w_down_e, *, out=None, stream=None):
+    """Parameter-average starting weights of the G united experts: (w_gate, w_up, w_down)."""
+    E, f, d = w_gate_e.shape
+    dt = w_gate_e.dtype
+    dtype = {torch.bfloat16: BMOE_BF16, torch.float32: BMOE_F32}[dt]
+    _dev(e2g, "e2g", torch.int32, (E,))
+    _dev(w_gate_e, "w_gate_e", dt, (E, f, d))
+    _dev(w_up_e, "w_up_e", dt, (E, f, d))
+    _dev(w_down_e, "w_down_e", dt, (E, d, f))
+    if out is None:
+        out = (_empty((G, f, d), dt, e2g.device), _empty((G, f, d), dt, e2g.device), _empty((G, d, f), dt, e2g.device))
+    for t, shp, nm in zip(out, ((G, f, d), (G, f, d), (G, d, f)), ("w_gate_u", "w_up_u", "w_down_u")):
+        _dev(t, nm, dt, shp)
+    st = load_library().brownout_moe_united_init(dtype, E, G, d, f, _p(e2g), _p(w_gate_e), _p(w_up_e), _p(w_down_e),
+                                                 _p(out[0]), _p(out[1]), _p(out[2]), _stream(stream))
+    _check(st, "brownout_moe_united_init")
+    return out
+
+
+def distill_mse(e2g: torch.Tensor, w_freq: torch.Tensor, y_expert: torch.Tensor, y_united: torch.Tensor, T: int,
+                *, workspace: Optional[torch.Tensor] = None, out=None, stream=None):
+    """(mse [G] float64, total [] float64) of Eq. 5-6 from the experts' outputs
+    [E*T, d] and the united experts' outputs [G*T, d] on T tokens."""
+    E = e2g.numel()
+    G = y_united.shape[0] // T if T else 0
+    d = y_expert.shape[1]
+    dt = y_expert.dtype
+    dtype = {torch.bfloat16: BMOE_BF16, torch.float32: BMOE_F32}[dt]
+    _dev(e2g, "e2g", torch.int32, (E,))
+    _dev(w_freq, "w_freq", torch.float32, (E,))
+    _dev(y_expert, "y_expert", dt, (E * T, d))
+    _dev(y_united, "y_united", dt, (G * T, d))
+    if workspace is None:
+        workspace = torch.empty(DISTILL_WS_BYTES, dtype=torch.uint8, device=e2g.device)
+    _dev(workspace, "workspace", torch.uint8)
+    mse, total = out if out is not None else (torch.zeros(G, dtype=torch.float64, device=e2g.device),
+                                              torch.zeros((), dtype=torch.float64, device=e2g.device))
+    st = load_library().brownout_moe_distill_mse(dtype, E, G, T, d, _p(e2g), _p(w_freq), _p(y_expert),
+                                                 _p(y_united), _p(mse), _p(total), _p(workspace),
+                                                 workspace.numel(), _stream(stream))
+    _check(st, "brownout_moe_distill_mse")
+    return mse, total
 
 
 def ffn_down(offsets, h, w_down, *, y=None, workspace=None, stream=None):

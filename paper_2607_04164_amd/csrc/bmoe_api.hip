@@ -179,6 +179,43 @@ bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t rows_cap
                       const_cast<void*>(h), y, workspace, workspace_bytes, stream);
 }
 
+bmoe_status brownout_moe_united_init(int32_t dtype, int32_t E, int32_t G, int32_t d, int32_t d_ff,
+                                     const int32_t* e2g, const void* w_gate_e, const void* w_up_e,
+                                     const void* w_down_e, void* w_gate_u, void* w_up_u, void* w_down_u,
+                                     void* stream) {
+    if (dtype != BMOE_F32 && dtype != BMOE_BF16) return BMOE_ERR_UNSUPPORTED;
+    if (E < 1 || E > BMOE_MAX_EXPERTS || G < 1 || G > BMOE_MAX_EXPERTS) return BMOE_ERR_SHAPE;
+    if (d < 8 || d % 8 != 0 || d_ff < 8 || d_ff % 8 != 0 || d > (1 << 20) || d_ff > (1 << 20))
+        return BMOE_ERR_SHAPE;
+    if (!e2g || !w_gate_e || !w_up_e || !w_down_e || !w_gate_u || !w_up_u || !w_down_u) return BMOE_ERR_NULL;
+    for (const void* p : {w_gate_e, w_up_e, w_down_e, (const void*)w_gate_u, (const void*)w_up_u,
+                          (const void*)w_down_u})
+        if (!aligned16(p)) return BMOE_ERR_ALIGN;
+    bmoe::UnitedInitArgs a{e2g, {w_gate_e, w_up_e, w_down_e}, {w_gate_u, w_up_u, w_down_u}, E, G, d, d_ff, dtype};
+    return hip_status(bmoe::launch_united_init(a, (hipStream_t)stream));
+}
+
+bmoe_status brownout_moe_distill_mse(int32_t dtype, int32_t E, int32_t G, int32_t T, int32_t d,
+                                     const int32_t* e2g, const float* w_freq, const void* y_expert,
+                                     const void* y_united, double* mse, double* mse_total, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+    if (dtype != BMOE_F32 && dtype != BMOE_BF16) return BMOE_ERR_UNSUPPORTED;
+    if (E < 1 || E > BMOE_MAX_EXPERTS || G < 1 || G > BMOE_MAX_EXPERTS || T < 0) return BMOE_ERR_SHAPE;
+    if (d < 8 || d % 8 != 0 || d > (1 << 20)) return BMOE_ERR_SHAPE;
+    if (T == 0) return BMOE_OK;
+    const int nb = bmoe::distill_blocks(G, T);
+    // the partial kernel indexes a workgroup's chunks with 32-bit ints
+    if ((int64_t)((T + nb - 1) / nb + 1) * (d / (dtype == BMOE_BF16 ? 8 : 4)) >= ((int64_t)1 << 31))
+        return BMOE_ERR_SHAPE;
+    if (!e2g || !w_freq || !y_expert || !y_united || !mse) return BMOE_ERR_NULL;
+    if (!aligned16(y_expert) || !aligned16(y_united) || ((uintptr_t)mse & 7u) || ((uintptr_t)mse_total & 7u))
+        return BMOE_ERR_ALIGN;
+    if (!workspace || workspace_bytes < (size_t)nb * G * sizeof(double)) return BMOE_ERR_WORKSPACE;
+    if ((uintptr_t)workspace & 7u) return BMOE_ERR_ALIGN;
+    bmoe::DistillArgs a{e2g, w_freq, y_expert, y_united, mse, mse_total, workspace, E, G, T, d, dtype};
+    return hip_status(bmoe::launch_distill_mse(a, (hipStream_t)stream));
+}
+
 bmoe_status brownout_moe_combine(const bmoe_desc* d, const int32_t* slot_row, const float* slot_gate,
                                  const void* y_perm, const void* y_shared, void* out, void* stream) {
     bmoe_status st = bmoe_validate(d);

@@ -132,6 +132,27 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* buf, int* to
 // Launchers implemented by the kernel files; arguments already validated.
 namespace bmoe {
 
+struct UnitedInitArgs {
+    const int32_t* e2g;
+    const void* src[3];  // member experts' W_gate, W_up [E, d_ff, d], W_down [E, d, d_ff]
+    void* dst[3];        // united experts' [G, ...]
+    int E, G, d, d_ff, dtype;
+};
+hipError_t launch_united_init(const UnitedInitArgs& a, hipStream_t s);
+
+struct DistillArgs {
+    const int32_t* e2g;
+    const float* w;         // routing frequencies [E]
+    const void* y_expert;   // [E*T, d]
+    const void* y_united;   // [G*T, d]
+    double* mse;            // [G]
+    double* total;          // nullable
+    void* ws;               // distill_blocks(G, T) * G doubles
+    int E, G, T, d, dtype;
+};
+int distill_blocks(int G, int T);
+hipError_t launch_distill_mse(const DistillArgs& a, hipStream_t s);
+
 struct RouteArgs {
     const void* x;
     const void* w;

@@ -133,6 +133,24 @@ def test_entry_points_reject_before_launch(lib):
     gu = lib.brownout_moe_ffn_gate_up_gather
     assert gu(1, 4, 128, 256, 512, FAKE, z, 64, FAKE, FAKE, FAKE, FAKE, z, 0, z) == NULL
     assert gu(1, 4, 128, 256, 512, FAKE, FAKE, 64, FAKE, FAKE, z, FAKE, z, 0, z) == NULL
+    # grouping search
+    ui = lib.brownout_moe_united_init
+    assert ui(9, 8, 4, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == UNSUP
+    assert ui(1, 0, 4, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert ui(1, 8, 257, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert ui(1, 8, 4, 250, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == SHAPE
+    assert ui(1, 8, 4, 256, 512, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == NULL
+    assert ui(1, 8, 4, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
+    dm = lib.brownout_moe_distill_mse
+    W = B.DISTILL_WS_BYTES
+    assert dm(9, 8, 4, 100, 256, FAKE, FAKE, FAKE, FAKE, FAKE, z, FAKE, W, z) == UNSUP
+    assert dm(1, 8, 4, -1, 256, FAKE, FAKE, FAKE, FAKE, FAKE, z, FAKE, W, z) == SHAPE
+    assert dm(1, 8, 4, 100, 260, FAKE, FAKE, FAKE, FAKE, FAKE, z, FAKE, W, z) == SHAPE
+    assert dm(1, 8, 4, 100, 256, FAKE, z, FAKE, FAKE, FAKE, z, FAKE, W, z) == NULL
+    assert dm(1, 8, 4, 100, 256, FAKE, FAKE, MISALIGNED, FAKE, FAKE, z, FAKE, W, z) == ALIGN
+    assert dm(1, 8, 4, 100, 256, FAKE, FAKE, FAKE, FAKE, FAKE, z, z, W, z) == WS
+    assert dm(1, 8, 4, 100, 256, FAKE, FAKE, FAKE, FAKE, FAKE, z, FAKE, 64, z) == WS
+    assert dm(1, 8, 4, 0, 256, z, z, z, z, z, z, z, 0, z) == OK
     # combine
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, z, z, z) == NULL
     assert lib.brownout_moe_combine(bd, FAKE, FAKE, FAKE, MISALIGNED, FAKE, z) == ALIGN
