@@ -280,9 +280,15 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
         return hipGetLastError();
     }
     const int nch = a.d * a.elem_bytes / 16;
-    hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
-                       a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
-                       a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
+    // a row of up to 8 KB in one batch of loads per lane
+    if (nch > 256)
+        hipLaunchKernelGGL(permute_kernel<8>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                           a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
+                           a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
+    else
+        hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                           a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
+                           a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
     return hipGetLastError();
 }
 
