@@ -335,6 +335,10 @@ constexpr int kGroupM = 4;
 #endif
 constexpr int kDmaBK = 64;
 constexpr int kSkPartBytes = 256 * 256 * 4;  // fp32 accumulators of one tile piece
+// workspace slot stride: a piece plus 1280 bytes, so that slots (which the
+// workgroups write, and the fixup reads, at the same offsets at the same
+// time) do not all start on the same memory channel
+constexpr int kSkSlotBytes = kSkPartBytes + 1280;
 
 template <bool GATED>
 struct DmaCfg {
@@ -689,26 +693,6 @@ __device__ __forceinline__ void store_piece(const f32x16 (&acc)[C::NMAT][C::MB][
                                     acc[mat][mb][nb][i + 3]);
 }
 
-template <class C>
-__device__ __forceinline__ void add_piece(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const char* slot) {
-    const float4* d = (const float4*)slot;
-    int q = 0;
-#pragma unroll
-    for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < C::NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 16; i += 4, ++q) {
-                    const float4 v = d[q * kGemmThreads + threadIdx.x];
-                    acc[mat][mb][nb][i] += v.x;
-                    acc[mat][mb][nb][i + 1] += v.y;
-                    acc[mat][mb][nb][i + 2] += v.z;
-                    acc[mat][mb][nb][i + 3] += v.w;
-                }
-}
-
 // Work of P persistent workgroups: F rounds of one tile each (round r, tile
 // r*P + w; the last round may be partial), then, split by K-steps, the tiles
 // [F*P, total): each workgroup gets `share` consecutive K-steps of those.
@@ -717,6 +701,7 @@ __device__ __forceinline__ void add_piece(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
 // whole tiles would leave the workgroups idle for more than min_idle K-steps
 // on average (kSkMinIdle unless BMOE_FFN_SPLIT_MIN_IDLE says otherwise).
 constexpr int kSkMinIdle = 48;
+constexpr int kSkMinShare = 8;  // K-steps: the shortest piece worth a pipeline restart
 struct SkSplit {
     int F, W, share;
 };
@@ -729,7 +714,12 @@ __device__ __forceinline__ SkSplit sk_split(int total, int nk, int P, bool can_s
         k.W = 0;
         k.share = 1;
     } else {
-        k.F = max(0, total / P - 1);
+        // split only the last partial round when its K-steps still give every
+        // workgroup a piece of kSkMinShare or more (fewer split tiles, fewer
+        // pieces through memory); otherwise the last one to two rounds
+        const int full = total / P;
+        const int64_t rest = (int64_t)(total - full * P) * nk;
+        k.F = rest >= (int64_t)kSkMinShare * P ? full : max(0, full - 1);
         k.W = (total - k.F * P) * nk;
         k.share = ceil_div(k.W, P);
     }
@@ -786,37 +776,113 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             zero_acc<C>(acc);
             tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane);
             if (slot < 0) store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
-            else store_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkPartBytes);
+            else store_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
         }
     }
 }
 
 // Sums the pieces of every tile that the stream-K split cut, in K order,
-// then applies the epilogue. Workgroup b looks at the share boundary b*share;
-// the first boundary inside a tile owns that tile.
+// then applies the epilogue. Workgroup (qs, b) looks at the share boundary
+// b*share; the first boundary inside a tile owns that tile, and qs picks one
+// of kFixSplit slices of the tile's accumulator slots, so a split tile is
+// finished by kFixSplit workgroups at once (one per tile streamed its pieces
+// through a single CU). Each thread adds its float4 slots of the pieces in
+// the order of the pieces, as the unsplit path would, and writes its four
+// rows of one column straight to the output.
+constexpr int kFixSplit = 16;
+
 template <bool GATED>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_fixup_kernel(GemmParams p, const char* ws, int P) {
+__global__ __launch_bounds__(kGemmThreads) void gemm_fixup_kernel(GemmParams p, const char* ws, int P) {
     using C = DmaCfg<GATED>;
-    __shared__ __align__(16) char smem[C::SMEM];
-    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-    const int b = blockIdx.x;
+    __shared__ __align__(16) char sched[C::SCHED];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int b = blockIdx.y, qs = blockIdx.x;  // the slices of one tile launch together
     if (b == 0) return;
-    const TileSched ts = tile_sched(p, smem + C::SCHED_OFF, C::BM, C::BN);
+    // the tile count first, by a plain sum (most workgroups own nothing and
+    // leave before the schedule's scan)
+    __shared__ int s_wsum[kGemmThreads / 64];
+    int cnt = 0;
+    if (tid < p.n_seg) {
+        const int beg = min(max(p.offsets[tid], 0), p.rows_cap);
+        const int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
+        cnt = ceil_div(end - beg, C::BM);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if (lane == 0) s_wsum[wave] = cnt;
+    __syncthreads();
+    const int total_mt = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
     const int nk = p.K / C::BK;
-    const SkSplit sk = sk_split(ts.total_mt * ts.NT, nk, P, true, p.sk_min_idle);
+    const SkSplit sk = sk_split(total_mt * ceil_div(p.N, C::BN), nk, P, true, p.sk_min_idle);
     const int q = b * sk.share;
     if (q >= sk.W || q % nk == 0) return;
     const int t = q / nk;
     if (b != t * nk / sk.share + 1) return;  // not the first boundary inside tile t
+    const TileSched ts = tile_sched(p, sched, C::BM, C::BN);
     const int p0 = t * nk / sk.share, p1 = ((t + 1) * nk - 1) / sk.share;
-    f32x16 acc[C::NMAT][C::MB][C::NB];
-    zero_acc<C>(acc);
-    for (int pw = p0; pw <= p1; ++pw) {
-        const int slot = pw * sk.share >= t * nk ? 0 : 1;  // share starts inside tile t, or ends in it
-        add_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkPartBytes);
-    }
     const TileCoord tc = tile_coord(ts, p.n_seg, sk.F * P + t, C::BM, C::BN);
-    store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
+    constexpr int NQ = C::MB * C::NB * 4;  // float4 slots of one matrix per thread
+    static_assert(NQ % kFixSplit == 0, "slices of whole slots");
+    constexpr int QPER = NQ / kFixSplit;
+    const int wm = wave >> 1, wn = wave & 1;
+    // all slots of this slice, piece after piece (every element still sums the
+    // pieces in order); four pieces' loads in flight per step
+    float4 sum[QPER][C::NMAT];
+#pragma unroll
+    for (int k = 0; k < QPER; ++k)
+#pragma unroll
+        for (int mat = 0; mat < C::NMAT; ++mat) sum[k][mat] = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto piece = [&](int pw) {
+        const int slot = pw * sk.share >= t * nk ? 0 : 1;  // share starts inside tile t, or ends in it
+        return (const float4*)(ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
+    };
+    auto add = [&](float4& a, const float4& v) {
+        a.x += v.x;
+        a.y += v.y;
+        a.z += v.z;
+        a.w += v.w;
+    };
+    int pw = p0;
+    for (; pw + 3 <= p1; pw += 4) {
+        float4 v[4][QPER][C::NMAT];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float4* d = piece(pw + j);
+#pragma unroll
+            for (int k = 0; k < QPER; ++k)
+#pragma unroll
+                for (int mat = 0; mat < C::NMAT; ++mat) v[j][k][mat] = d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int k = 0; k < QPER; ++k)
+#pragma unroll
+                for (int mat = 0; mat < C::NMAT; ++mat) add(sum[k][mat], v[j][k][mat]);
+    }
+    for (; pw <= p1; ++pw) {
+        const float4* d = piece(pw);
+#pragma unroll
+        for (int k = 0; k < QPER; ++k)
+#pragma unroll
+            for (int mat = 0; mat < C::NMAT; ++mat) add(sum[k][mat], d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid]);
+    }
+#pragma unroll
+    for (int k = 0; k < QPER; ++k) {
+        const int qq = qs * QPER + k;  // slot (mb, nb, i4) in the order of store_piece
+        const int i4 = qq & 3, nb = (qq >> 2) % C::NB, mb = (qq >> 2) / C::NB;
+        const int r0 = wm * C::WTM + mb * 32 + 8 * i4 + 4 * (lane >> 5);
+        const int gn = tc.n0 + wn * C::WTN + nb * 32 + (lane & 31);
+        const float g4[4] = {sum[k][0].x, sum[k][0].y, sum[k][0].z, sum[k][0].w};
+        const float4 u = sum[k][C::NMAT - 1];
+        const float u4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float v = GATED ? silu_mul(g4[j], u4[j]) : g4[j];
+            const int gm = tc.m0 + r0 + j;
+            if (gm < tc.m_end && gn < p.N) p.C[(size_t)gm * p.N + gn] = (uint16_t)pack_bf16x2_hw(v, 0.f);
+        }
+    }
 }
 
 // CUs of the current device, rounded down to a multiple of 8 (XCD deal)
@@ -847,12 +913,13 @@ hipError_t launch_gemm_dma(const GemmParams& g0, void* ws, size_t ws_bytes, hipS
     // persistent: one workgroup per CU, each XCD a contiguous range of tiles
     const int P = stream_k_workgroups();
     if (P > 0) {
-        const bool split = ws != nullptr && ws_bytes >= (size_t)2 * P * kSkPartBytes;
+        const bool split = ws != nullptr && ws_bytes >= (size_t)2 * P * kSkSlotBytes;
         hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, true>), dim3(P), dim3(kGemmThreads), 0, s, g,
                            split ? (char*)ws : (char*)nullptr);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess || !split) return e;
-        hipLaunchKernelGGL((gemm_fixup_kernel<GATED>), dim3(P), dim3(kGemmThreads), 0, s, g, (const char*)ws, P);
+        hipLaunchKernelGGL((gemm_fixup_kernel<GATED>), dim3(kFixSplit, P), dim3(kGemmThreads), 0, s, g,
+                           (const char*)ws, P);
         return hipGetLastError();
     }
     const int64_t mt_max = ceil_div64(g.rows_cap, C::BM) + g.n_seg;
@@ -919,7 +986,7 @@ __global__ __launch_bounds__(256) void ffn_f32_down_kernel(const float* __restri
 
 size_t ffn_workspace_bytes() {
     const int P = stream_k_workgroups();
-    return P > 0 ? (size_t)2 * P * kSkPartBytes : 0;
+    return P > 0 ? (size_t)2 * P * kSkSlotBytes : 0;
 }
 
 // Workgroup tile of the bf16 grouped GEMMs. 256-row tiles (128x128 per wave)
