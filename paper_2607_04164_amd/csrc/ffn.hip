@@ -541,8 +541,13 @@ __device__ __forceinline__ TileCoord tile_coord(const TileSched& t, int n_seg, i
 
 template <class C, bool GATED>
 __device__ __forceinline__ void dma_sources(DmaSrc<C>& src, const GemmParams& p, const TileCoord& tc, int wave,
-                                            int lane) {
+                                            int lane_in) {
     const int K = p.K, N = p.N;
+    // the lane-dependent parts are recomputed for every tile (a few integer
+    // operations): held across the persistent loop they were spilled to
+    // scratch and reloaded one dependent load at a time
+    int lane = lane_in;
+    asm volatile("" : "+v"(lane));
     const int lrow = lane / C::KC, lchk = lane % C::KC;
     // offsets from the tile's first row, or from row 0 of the source when the
     // rows are gathered (the host keeps a_count * K * 2 below 2^32)
@@ -634,27 +639,59 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[C::NMAT][C::MB][C::NB]) {
                 for (int i = 0; i < 16; ++i) acc[mat][mb][nb][i] = 0.f;
 }
 
+// An accumulator moved out of its AGPR at the point of use (the compiler
+// otherwise copies every accumulator to VGPRs at once after the K loop and,
+// inside the persistent loop, spills to scratch).
+template <bool FORCE>
+__device__ __forceinline__ float acc_read(float a) {
+    if constexpr (!FORCE) return a;  // the down GEMM's epilogue fits without it (and ran faster so)
+    float v;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
+    return v;
+}
+
 // Epilogue: the wave's tile (SiLU(gate)*up for the gated GEMM) is staged in
-// LDS as bf16, then written with 128-bit row stores. Ends with a barrier.
+// LDS as bf16, then written with 128-bit row stores; or, with a piece slot,
+// the raw fp32 accumulators go to the slot (lane-interleaved float4, the
+// layout the fixup reads). One routine for both, block by block: with two
+// routines the compiler moved every accumulator out of the AGPRs where the
+// paths split and spilled. Ends with a barrier.
 template <class C, bool GATED>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], const GemmParams& p,
-                                           const TileCoord& tc, char* smem, int wave, int lane) {
+                                           const TileCoord& tc, char* smem, int wave, int lane,
+                                           char* piece = nullptr) {
     const int wm = wave >> 1, wn = wave & 1;
     uint16_t* st = (uint16_t*)smem + (size_t)wave * C::WTM * C::SROW;
     const int l32 = lane & 31;
+    // one 32x32 block at a time (scheduling fences): moving every accumulator
+    // out of the AGPRs at once ran out of VGPRs and spilled to scratch
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < C::NB; ++nb)
+        for (int nb = 0; nb < C::NB; ++nb) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (piece) {
+                float4* d = (float4*)piece;
+#pragma unroll
+                for (int mat = 0; mat < C::NMAT; ++mat)
+#pragma unroll
+                    for (int i = 0; i < 16; i += 4) {
+                        const int q = ((mat * C::MB + mb) * C::NB + nb) * 4 + i / 4;
+                        d[q * kGemmThreads + threadIdx.x] =
+                            make_float4(acc_read<GATED>(acc[mat][mb][nb][i]), acc_read<GATED>(acc[mat][mb][nb][i + 1]),
+                                        acc_read<GATED>(acc[mat][mb][nb][i + 2]), acc_read<GATED>(acc[mat][mb][nb][i + 3]));
+                    }
+                continue;
+            }
 #pragma unroll
             for (int i = 0; i < 16; i += 2) {
                 float v0, v1;
                 if constexpr (GATED) {
-                    v0 = silu_mul(acc[0][mb][nb][i], acc[1][mb][nb][i]);
-                    v1 = silu_mul(acc[0][mb][nb][i + 1], acc[1][mb][nb][i + 1]);
+                    v0 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i]), acc_read<GATED>(acc[1][mb][nb][i]));
+                    v1 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i + 1]), acc_read<GATED>(acc[1][mb][nb][i + 1]));
                 } else {
-                    v0 = acc[0][mb][nb][i];
-                    v1 = acc[0][mb][nb][i + 1];
+                    v0 = acc_read<GATED>(acc[0][mb][nb][i]);
+                    v1 = acc_read<GATED>(acc[0][mb][nb][i + 1]);
                 }
                 const uint32_t pk = pack_bf16x2_hw(v0, v1);
                 const int r = mb * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
@@ -662,6 +699,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
                 st[r * C::SROW + c] = (uint16_t)pk;
                 st[(r + 1) * C::SROW + c] = (uint16_t)(pk >> 16);
             }
+        }
+    __builtin_amdgcn_sched_barrier(0);
+    if (piece) return;  // (uniform) no LDS staging, no barrier needed
     __syncthreads();
     constexpr int CPR = C::WTN / 8;
     const int row0 = tc.m0 + wm * C::WTM, col0 = tc.n0 + wn * C::WTN;
@@ -673,24 +713,6 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
             *(uint4*)(p.C + (size_t)gm * p.N + gn) = *(const uint4*)(st + r * C::SROW + cc * 8);
     }
     __syncthreads();
-}
-
-// fp32 accumulators of a tile piece, lane-interleaved float4 (coalesced)
-template <class C>
-__device__ __forceinline__ void store_piece(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], char* slot) {
-    float4* d = (float4*)slot;
-    int q = 0;
-#pragma unroll
-    for (int mat = 0; mat < C::NMAT; ++mat)
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < C::NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 16; i += 4, ++q)
-                    d[q * kGemmThreads + threadIdx.x] =
-                        make_float4(acc[mat][mb][nb][i], acc[mat][mb][nb][i + 1], acc[mat][mb][nb][i + 2],
-                                    acc[mat][mb][nb][i + 3]);
 }
 
 // Work of P persistent workgroups: F rounds of one tile each (round r, tile
@@ -775,8 +797,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             dma_sources<C, GATED>(src, p, tc, wave, lane);
             zero_acc<C>(acc);
             tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane);
-            if (slot < 0) store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
-            else store_piece<C>(acc, ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
+            store_tile<C, GATED>(acc, p, tc, smem, wave, lane,
+                                 slot < 0 ? nullptr : ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
         }
     }
 }
