@@ -357,11 +357,15 @@ struct DmaCfg {
     static constexpr int A_STAGE = BM * ROW_BYTES, B_STAGE = RB * ROW_BYTES;
     static constexpr int STAGE = A_STAGE + B_STAGE;
     static constexpr int SROW = WTN + 8;
-    static constexpr int EPI = 4 * WTM * SROW * 2;
     static constexpr int RING = 2 * STAGE;
-    static constexpr int SCHED_OFF = RING > EPI ? RING : EPI;             // schedule arrays live after
-    static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;   // the ring / staging area
+    // epilogue staging: each wave its own 16 rows x WTN, outside the ring, so
+    // the next tile's first copies can land while a tile's results go out
+    static constexpr int HSTG = 16 * SROW * 2;
+    static constexpr int STG_OFF = RING;
+    static constexpr int SCHED_OFF = STG_OFF + 4 * HSTG;                 // schedule arrays after them
+    static constexpr int SCHED = (256 + 3 * BMOE_MAX_EXPERTS + 1) * 4;
     static constexpr int SMEM = SCHED_OFF + SCHED;
+    static constexpr int CPR = WTN / 8;                                   // 16-byte chunks per output row
     static constexpr int NACC4 = NMAT * MB * NB * 4;                      // float4 accumulators per lane
     static_assert(KC == 8 && BM == 256 && RB == 256, "tile shape");
     static_assert(SUB % 2 == 0, "fragment double buffer alternates within a K-step");
@@ -571,18 +575,33 @@ __device__ __forceinline__ void dma_sources(DmaSrc<C>& src, const GemmParams& p,
     }
 }
 
-// K-steps [ka, kb) of one tile into acc (which the caller zeroed). Ends with
-// every copy complete and a barrier, so the LDS may be reused.
+// The copies of K-steps ka and ka+1 (when the item has two) into the ring's
+// two slots; the ring must be free (every wave done reading it).
+template <class C>
+__device__ __forceinline__ void ksteps_prologue(const DmaSrc<C>& src, char* smem, int ka, int kb, int wave) {
+    const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    dma_stage<C>(src, lds0, wave, ka * C::BK * 2);
+    if (kb - ka > 1) dma_stage<C>(src, lds0 + C::STAGE, wave, (ka + 1) * C::BK * 2);
+}
+
+// What a wave issued to vector memory after its prologue copies: nothing, or
+// the previous item's epilogue stores. The first wait then counts only the
+// second K-step's copies, or waits for everything (stores included: the
+// counter is not relied on to order the copies before later stores).
+enum { kAfterNone = 0, kAfterStores = 1 };
+
+// K-steps [ka, kb) of one tile into acc (which the caller zeroed), after
+// ksteps_prologue. Ends with every copy complete and a barrier, so the LDS
+// ring may be reused.
 template <class C>
 __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
-                                            char* smem, int ka, int kb, int wave, int lane) {
+                                            char* smem, int ka, int kb, int wave, int lane, int after) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
     const int wm = wave >> 1, wn = wave & 1;
     const int n = kb - ka;
-    // prologue: K-steps ka and ka+1 in flight, wait for ka
-    dma_stage<C>(src, lds0, wave, ka * C::BK * 2);
-    if (n > 1) dma_stage<C>(src, lds0 + C::STAGE, wave, (ka + 1) * C::BK * 2);
-    if (n > 1) wait_vmcnt<C::DMA_PER_STAGE>();
+    // wait for K-step ka: vector-memory operations complete in issue order, so
+    // at most (its successors) may still be outstanding
+    if (after == kAfterNone && n > 1) wait_vmcnt<C::DMA_PER_STAGE>();
     else wait_vmcnt<0>();
     wg_barrier();
     uint4 af0[C::MB], af1[C::MB];
@@ -650,28 +669,29 @@ __device__ __forceinline__ float acc_read(float a) {
     return v;
 }
 
-// Epilogue: the wave's tile (SiLU(gate)*up for the gated GEMM) is staged in
-// LDS as bf16, then written with 128-bit row stores; or, with a piece slot,
-// the raw fp32 accumulators go to the slot (lane-interleaved float4, the
-// layout the fixup reads). One routine for both, block by block: with two
-// routines the compiler moved every accumulator out of the AGPRs where the
-// paths split and spilled. Ends with a barrier.
+// Epilogue: the wave's tile (SiLU(gate)*up for the gated GEMM) goes out 16
+// rows at a time: staged as bf16 in the wave's own LDS area (outside the
+// copy ring), read back in 16-byte row chunks and stored with 128-bit
+// stores, with no workgroup barrier.
+// With a piece slot instead, the raw fp32 accumulators go to the slot
+// (lane-interleaved float4, the layout the fixup reads). One routine for
+// both, block by block: with two routines the compiler moved every
+// accumulator out of the AGPRs where the paths split and spilled.
 template <class C, bool GATED>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], const GemmParams& p,
                                            const TileCoord& tc, char* smem, int wave, int lane,
                                            char* piece = nullptr) {
     const int wm = wave >> 1, wn = wave & 1;
-    uint16_t* st = (uint16_t*)smem + (size_t)wave * C::WTM * C::SROW;
+    uint16_t* st = (uint16_t*)(smem + C::STG_OFF + wave * C::HSTG);
     const int l32 = lane & 31;
-    // one 32x32 block at a time (scheduling fences): moving every accumulator
-    // out of the AGPRs at once ran out of VGPRs and spilled to scratch
+    const int row0 = tc.m0 + wm * C::WTM, col0 = tc.n0 + wn * C::WTN;
+    if (piece) {
+        float4* d = (float4*)piece;
 #pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
+        for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < C::NB; ++nb) {
-            __builtin_amdgcn_sched_barrier(0);
-            if (piece) {
-                float4* d = (float4*)piece;
+            for (int nb = 0; nb < C::NB; ++nb) {
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int mat = 0; mat < C::NMAT; ++mat)
 #pragma unroll
@@ -679,40 +699,48 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
                         const int q = ((mat * C::MB + mb) * C::NB + nb) * 4 + i / 4;
                         d[q * kGemmThreads + threadIdx.x] =
                             make_float4(acc_read<GATED>(acc[mat][mb][nb][i]), acc_read<GATED>(acc[mat][mb][nb][i + 1]),
-                                        acc_read<GATED>(acc[mat][mb][nb][i + 2]), acc_read<GATED>(acc[mat][mb][nb][i + 3]));
+                                        acc_read<GATED>(acc[mat][mb][nb][i + 2]),
+                                        acc_read<GATED>(acc[mat][mb][nb][i + 3]));
                     }
-                continue;
             }
+        return;
+    }
 #pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                float v0, v1;
-                if constexpr (GATED) {
-                    v0 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i]), acc_read<GATED>(acc[1][mb][nb][i]));
-                    v1 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i + 1]), acc_read<GATED>(acc[1][mb][nb][i + 1]));
-                } else {
-                    v0 = acc_read<GATED>(acc[0][mb][nb][i]);
-                    v1 = acc_read<GATED>(acc[0][mb][nb][i + 1]);
+    for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // rows 16h .. 16h+15 of the 32-row block: accumulator elements 8h .. 8h+7
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                for (int i = 8 * h; i < 8 * h + 8; i += 2) {
+                    float v0, v1;
+                    if constexpr (GATED) {
+                        v0 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i]), acc_read<GATED>(acc[1][mb][nb][i]));
+                        v1 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i + 1]), acc_read<GATED>(acc[1][mb][nb][i + 1]));
+                    } else {
+                        v0 = acc_read<GATED>(acc[0][mb][nb][i]);
+                        v1 = acc_read<GATED>(acc[0][mb][nb][i + 1]);
+                    }
+                    const uint32_t pk = pack_bf16x2_hw(v0, v1);
+                    const int r = 8 * ((i >> 2) - 2 * h) + 4 * (lane >> 5) + (i & 3);
+                    const int c = nb * 32 + l32;
+                    st[r * C::SROW + c] = (uint16_t)pk;
+                    st[(r + 1) * C::SROW + c] = (uint16_t)(pk >> 16);
                 }
-                const uint32_t pk = pack_bf16x2_hw(v0, v1);
-                const int r = mb * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-                const int c = nb * 32 + l32;
-                st[r * C::SROW + c] = (uint16_t)pk;
-                st[(r + 1) * C::SROW + c] = (uint16_t)(pk >> 16);
+            // the wave reads back only what it wrote (LDS operations of a wave
+            // complete in order), then the next half block reuses the area
+#pragma unroll
+            for (int k = 0; k < 16 * C::CPR / 64; ++k) {
+                const int c = lane + 64 * k;
+                const int rr = c / C::CPR, cc = c % C::CPR;
+                const int gm = row0 + mb * 32 + 16 * h + rr, gn = col0 + cc * 8;
+                const uint4 v = *(const uint4*)(st + rr * C::SROW + cc * 8);
+                if (gm < tc.m_end && gn < p.N) *(uint4*)(p.C + (size_t)gm * p.N + gn) = v;
             }
         }
     __builtin_amdgcn_sched_barrier(0);
-    if (piece) return;  // (uniform) no LDS staging, no barrier needed
-    __syncthreads();
-    constexpr int CPR = C::WTN / 8;
-    const int row0 = tc.m0 + wm * C::WTM, col0 = tc.n0 + wn * C::WTN;
-#pragma unroll 4
-    for (int c = lane; c < C::WTM * CPR; c += 64) {
-        const int r = c / CPR, cc = c % CPR;
-        const int gm = row0 + r, gn = col0 + cc * 8;
-        if (gm < tc.m_end && gn < p.N)
-            *(uint4*)(p.C + (size_t)gm * p.N + gn) = *(const uint4*)(st + r * C::SROW + cc * 8);
-    }
-    __syncthreads();
 }
 
 // Work of P persistent workgroups: F rounds of one tile each (round r, tile
@@ -764,7 +792,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         const TileCoord tc = tile_coord(ts, p.n_seg, L, C::BM, C::BN);
         dma_sources<C, GATED>(src, p, tc, wave, lane);
         zero_acc<C>(acc);
-        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane);
+        ksteps_prologue<C>(src, smem, 0, nk, wave);
+        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone);
         store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
     } else {
         const int P = gridDim.x;
@@ -774,15 +803,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         // of the remaining K-steps; one loop so every stage is inlined once
         const int i0 = min(sk.W, pw * sk.share), i1 = min(sk.W, i0 + sk.share);
         int r = 0, i = i0;
-        while (true) {
-            int L, ka, kb, slot = -1;
-            if (r < sk.F) {
+        // the next work item (L < 0: none left)
+        auto next_item = [&](int& L, int& ka, int& kb, int& slot) {
+            slot = -1;
+            while (r < sk.F) {
                 L = r * P + pw;
                 ka = 0;
                 kb = nk;
                 ++r;
-                if (L >= total) continue;  // last whole-tile round is partial
-            } else if (i < i1) {
+                if (L < total) return;  // the last whole-tile round may be partial
+            }
+            if (i < i1) {
                 const int t = i / nk;
                 ka = i - t * nk;
                 kb = min(nk, ka + (i1 - i));
@@ -790,15 +821,40 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
                 // slot 0: the piece that starts the share, slot 1: the one that ends it
                 if (ka != 0 || kb != nk) slot = i == i0 ? 0 : 1;
                 i += kb - ka;
-            } else {
-                break;
+                return;
             }
-            const TileCoord tc = tile_coord(ts, p.n_seg, L, C::BM, C::BN);
+            L = -1;
+        };
+        // The next item's first copies are issued before this item's results
+        // go out, so they land while the epilogue runs.
+        int L, ka, kb, slot;
+        next_item(L, ka, kb, slot);
+        TileCoord tc;
+        if (L >= 0) {
+            tc = tile_coord(ts, p.n_seg, L, C::BM, C::BN);
             dma_sources<C, GATED>(src, p, tc, wave, lane);
+            ksteps_prologue<C>(src, smem, ka, kb, wave);
+        }
+        int after = kAfterNone;
+        while (L >= 0) {
             zero_acc<C>(acc);
-            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane);
+            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane, after);
+            int L2, ka2, kb2, slot2;
+            next_item(L2, ka2, kb2, slot2);
+            TileCoord tc2;
+            if (L2 >= 0) {
+                tc2 = tile_coord(ts, p.n_seg, L2, C::BM, C::BN);
+                dma_sources<C, GATED>(src, p, tc2, wave, lane);
+                ksteps_prologue<C>(src, smem, ka2, kb2, wave);
+            }
             store_tile<C, GATED>(acc, p, tc, smem, wave, lane,
                                  slot < 0 ? nullptr : ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
+            after = kAfterStores;
+            L = L2;
+            ka = ka2;
+            kb = kb2;
+            slot = slot2;
+            tc = tc2;
         }
     }
 }
