@@ -20,6 +20,7 @@
 //
 // f32 path (small correctness configurations): one output element per thread.
 #include <cstdlib>
+#include <type_traits>
 
 #include "bmoe_common.h"
 
@@ -460,12 +461,14 @@ __device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C
 
 // The MFMAs of one sub-step with the wave's DMA instructions of a K-step
 // spread between them, so that a DMA issue that waits for queue space does
-// not hold back a run of MFMAs. Only the asm copy sits behind the (uniform)
-// branch: MFMAs under control flow make the compiler shuffle accumulators.
-template <class C>
+// not hold back a run of MFMAs. DMA is a template argument: the K loop runs
+// as a main part that always copies and a two-step tail that never does, so
+// no copy sits behind a branch (a uniform branch per copy was 13x the
+// branches of a library GEMM of the same shape).
+template <class C, bool DMA>
 __device__ __forceinline__ void mfmas_with_dma(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
                                                const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
-                                               uint32_t stage_lds, int wave, int kb, bool do_dma) {
+                                               uint32_t stage_lds, int wave, int kb) {
     constexpr int NM = C::NMAT * C::MB * C::NB;
     static_assert(C::DMA_PER_STAGE == NM, "one DMA per MFMA");
 #pragma unroll
@@ -473,7 +476,7 @@ __device__ __forceinline__ void mfmas_with_dma(f32x16 (&acc)[C::NMAT][C::MB][C::
         const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
         acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
         __builtin_amdgcn_sched_barrier(0);
-        if (do_dma) dma_one<C>(src, stage_lds, wave, kb, q);
+        if constexpr (DMA) dma_one<C>(src, stage_lds, wave, kb, q);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -613,7 +616,8 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
     // sched_barrier(0) fences keep each group of fragment reads ahead of the
     // MFMA group that hides its latency.
-    for (int kt = 0; kt < n; ++kt) {
+    auto kstep = [&](int kt, auto with_dma) {
+        constexpr bool DMA = decltype(with_dma)::value;
         const int slot = kt & 1;
         const char* stage = smem + slot * C::STAGE;
 #pragma unroll
@@ -627,14 +631,13 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
             // released by the barrier of the previous sub-step); the others
             // carry the fragment reads of the next sub-step
             if (j == C::SUB - 1)  // resolved by the unrolling
-                mfmas_with_dma<C>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (ka + kt + 2) * C::BK * 2,
-                                  kt + 2 < n);
+                mfmas_with_dma<C, DMA>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (ka + kt + 2) * C::BK * 2);
             else
                 mfmas_with_reads<C>(acc, fa, fb, ga, gb, stage, wm, wn, lane, j + 1);
             __builtin_amdgcn_sched_barrier(0);
             if (j == C::SUB - 2) {
-                // copies issued so far: K-steps up to min(n-1, kt+1); kt+1 must be resident
-                if (kt + 1 < n) wait_vmcnt<0>();
+                // every copy issued so far (K-steps up to kt+1) must be resident
+                wait_vmcnt<0>();
                 lds_reads_done();
                 wg_barrier();
                 // registers of this sub-step are free now: next K-step, sub-step 0
@@ -642,7 +645,10 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-    }
+    };
+    int kt = 0;
+    for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
+    for (; kt < n; ++kt) kstep(kt, std::false_type{});
     __syncthreads();
 }
 
@@ -661,9 +667,7 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[C::NMAT][C::MB][C::NB]) {
 // An accumulator moved out of its AGPR at the point of use (the compiler
 // otherwise copies every accumulator to VGPRs at once after the K loop and,
 // inside the persistent loop, spills to scratch).
-template <bool FORCE>
 __device__ __forceinline__ float acc_read(float a) {
-    if constexpr (!FORCE) return a;  // the down GEMM's epilogue fits without it (and ran faster so)
     float v;
     asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
     return v;
@@ -698,9 +702,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
                     for (int i = 0; i < 16; i += 4) {
                         const int q = ((mat * C::MB + mb) * C::NB + nb) * 4 + i / 4;
                         d[q * kGemmThreads + threadIdx.x] =
-                            make_float4(acc_read<GATED>(acc[mat][mb][nb][i]), acc_read<GATED>(acc[mat][mb][nb][i + 1]),
-                                        acc_read<GATED>(acc[mat][mb][nb][i + 2]),
-                                        acc_read<GATED>(acc[mat][mb][nb][i + 3]));
+                            make_float4(acc_read(acc[mat][mb][nb][i]), acc_read(acc[mat][mb][nb][i + 1]),
+                                        acc_read(acc[mat][mb][nb][i + 2]),
+                                        acc_read(acc[mat][mb][nb][i + 3]));
                     }
             }
         return;
@@ -717,11 +721,11 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
                 for (int i = 8 * h; i < 8 * h + 8; i += 2) {
                     float v0, v1;
                     if constexpr (GATED) {
-                        v0 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i]), acc_read<GATED>(acc[1][mb][nb][i]));
-                        v1 = silu_mul(acc_read<GATED>(acc[0][mb][nb][i + 1]), acc_read<GATED>(acc[1][mb][nb][i + 1]));
+                        v0 = silu_mul(acc_read(acc[0][mb][nb][i]), acc_read(acc[1][mb][nb][i]));
+                        v1 = silu_mul(acc_read(acc[0][mb][nb][i + 1]), acc_read(acc[1][mb][nb][i + 1]));
                     } else {
-                        v0 = acc_read<GATED>(acc[0][mb][nb][i]);
-                        v1 = acc_read<GATED>(acc[0][mb][nb][i + 1]);
+                        v0 = acc_read(acc[0][mb][nb][i]);
+                        v1 = acc_read(acc[0][mb][nb][i + 1]);
                     }
                     const uint32_t pk = pack_bf16x2_hw(v0, v1);
                     const int r = 8 * ((i >> 2) - 2 * h) + 4 * (lane >> 5) + (i & 3);
