@@ -38,8 +38,8 @@ VALU_F32_PEAK_TFLOPS = 157.3
 # --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
 # all of them). Valid only for the kernel sources they were taken with.
 TRAFFIC_RECORDS = {
-    "mixtral": {"src_sha1": "876e1fbc0fdad926afa1f2d745575ee3a0e4a98b",
-                "fetch_kib": 1658967.4, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "mixtral": {"src_sha1": "3601ec5011faf6e78a8e06b02d7be8ae7d8e12a2",
+                "fetch_kib": 1660066.4, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
                 "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
 }
 TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
