@@ -544,6 +544,22 @@ def test_layer_fused_gather(name):
     check_layer(L, ref, layer, out1)
 
 
+@pytest.mark.parametrize("name", ["mixtral", "fine", "heavy", "decode"])
+def test_full_size_fused_gather_bit_identical(name):
+    """At full size and with the stream-K workspace, the fused-gather layer
+    writes the same bits as the four-call layer (whose parity with the oracle
+    test_full_size_sampled checks)."""
+    L = full_case(name)
+    cfg = L.cfg
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    out0 = B.LayerForward(desc_of(cfg), w)(x).clone()
+    layer = B.LayerForward(desc_of(cfg), w, fused_gather=True)
+    out1 = layer(x)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out0)
+
+
 # ---------------------------------------------------------------------------
 # one GPU's share of a layer sharded over several GPUs
 
