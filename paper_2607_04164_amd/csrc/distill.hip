@@ -139,24 +139,46 @@ __global__ __launch_bounds__(kDThreads) void distill_partial_kernel(const int32_
     const int nc = (t1 - t0) * nch;  // chunks of this workgroup (the host bounds T d / nb)
     double acc = 0.0;
     if (n > 0) {
-        for (int c = threadIdx.x; c < nc; c += kDThreads) {
-            const int t = t0 + c / nch, j = c % nch;
-            float tv[EPC];
+        // two chunks per thread and step, every load of both issued before any
+        // is used; squares added in chunk order
+        constexpr int U = 2;
+        for (int c0 = threadIdx.x; c0 < nc; c0 += U * kDThreads) {
+            float tv[U][EPC], u[U][EPC];
 #pragma unroll
-            for (int i = 0; i < EPC; ++i) tv[i] = 0.f;
+            for (int q = 0; q < U; ++q)
+#pragma unroll
+                for (int i = 0; i < EPC; ++i) tv[q][i] = 0.f;
+            bool ok[U];
+            int t[U], j[U];
+#pragma unroll
+            for (int q = 0; q < U; ++q) {
+                const int c = c0 + q * kDThreads;
+                ok[q] = c < nc;
+                const int cc = ok[q] ? c : 0;
+                t[q] = t0 + cc / nch;
+                j[q] = cc % nch;
+            }
             for (int m = 0; m < n; ++m) {
-                float v[EPC];
-                load_chunk<V>(y_e + ((size_t)s_mem[m] * T + t) * d + (size_t)j * EPC, v);
+                float v[U][EPC];
+#pragma unroll
+                for (int q = 0; q < U; ++q)
+                    load_chunk<V>(y_e + ((size_t)s_mem[m] * T + t[q]) * d + (size_t)j[q] * EPC, v[q]);
                 const float a = s_alpha[m];
 #pragma unroll
-                for (int i = 0; i < EPC; ++i) tv[i] = fmaf(a, v[i], tv[i]);
-            }
-            float u[EPC];
-            load_chunk<V>(y_u + ((size_t)r * T + t) * d + (size_t)j * EPC, u);
+                for (int q = 0; q < U; ++q)
 #pragma unroll
-            for (int i = 0; i < EPC; ++i) {
-                const double df = (double)(u[i] - tv[i]);
-                acc = fma(df, df, acc);
+                    for (int i = 0; i < EPC; ++i) tv[q][i] = fmaf(a, v[q][i], tv[q][i]);
+            }
+#pragma unroll
+            for (int q = 0; q < U; ++q) load_chunk<V>(y_u + ((size_t)r * T + t[q]) * d + (size_t)j[q] * EPC, u[q]);
+#pragma unroll
+            for (int q = 0; q < U; ++q) {
+                if (!ok[q]) continue;
+#pragma unroll
+                for (int i = 0; i < EPC; ++i) {
+                    const double df = (double)(u[q][i] - tv[q][i]);
+                    acc = fma(df, df, acc);
+                }
             }
         }
     }
@@ -203,8 +225,9 @@ __global__ __launch_bounds__(kDThreads) void distill_final_kernel(const int32_t*
 }  // namespace
 
 int distill_blocks(int G, int T) {
-    // enough workgroups to fill the chip, at most one per token
-    int nb = (2048 + G - 1) / G;
+    // about four workgroups per CU (measured: 512 or 2048 in all were slower),
+    // at most one per token
+    int nb = (1024 + G - 1) / G;
     return nb < T ? nb : T;
 }
 
