@@ -38,8 +38,8 @@ VALU_F32_PEAK_TFLOPS = 157.3
 # --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
 # all of them). Valid only for the kernel sources they were taken with.
 TRAFFIC_RECORDS = {
-    "mixtral": {"src_sha1": "3601ec5011faf6e78a8e06b02d7be8ae7d8e12a2",
-                "fetch_kib": 1660066.4, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "mixtral": {"src_sha1": "4dd1e932f71a7428a491c23a6acd35d9e2be47e7",
+                "fetch_kib": 1610999.1, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
                 "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
 }
 TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
@@ -350,13 +350,18 @@ def main():
 
     # algorithmic work per launch
     T, d, E, k, f, s = cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.d_ff, cfg.elem_bytes
+    # The library streams the weights through the skinny kernel when the bf16
+    # FFN's row capacity (T*k) averages at most 64 rows per segment; that
+    # kernel is bound by the weight bytes of the segments that have rows.
+    skinny = cfg.dtype == "bf16" and T * k <= 64 * len(counts)
+    S_w = sum(1 for c in counts if c > 0)
     work = {
         "route": ("hbm", T * d * s + E * d * s + T * k * 16),
         # fused gather: the permutation only (slot_group in, slot_row and perm_token out)
         "dispatch": ("hbm", (T * k * 8 + N * 4) if args.fused_gather else
                      (T * k * 4 + T * d * s + N * d * s + N * 4 + T * k * 4)),
-        "ffn_gate_up": ("mfma", 4.0 * N * d * f),
-        "ffn_down": ("mfma", 2.0 * N * d * f),
+        "ffn_gate_up": ("hbm", 2 * S_w * d * f * s + N * d * s + N * f * s) if skinny else ("mfma", 4.0 * N * d * f),
+        "ffn_down": ("hbm", S_w * d * f * s + N * f * s + N * d * s) if skinny else ("mfma", 2.0 * N * d * f),
         "shared_ffn": ("mfma", 6.0 * T * d * cfg.d_ff_shared),
         "combine": ("hbm", T * k * 8 + N * d * s + T * d * s * (2 if cfg.n_shared else 1)),
     }
@@ -369,12 +374,13 @@ def main():
         ms = iso_ms[st_name]
         if kind == "hbm":
             rate = amount / (ms * 1e-3) / 1e9
-            cold = amount / (cold_ms[st_name] * 1e-3) / 1e9
             stage_out[st_name] = {"us": round(ms * 1e3, 2), "in_step_us": round(per_stage_ms[st_name] * 1e3, 2),
                                   "bytes": int(amount), "GB_s": round(rate, 1),
-                                  "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4),
-                                  "cold_us": round(cold_ms[st_name] * 1e3, 2), "cold_GB_s": round(cold, 1),
-                                  "cold_frac_of_hbm_peak": round(cold / HBM_PEAK_GBS, 4)}
+                                  "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+            if st_name in cold_ms:
+                cold = amount / (cold_ms[st_name] * 1e-3) / 1e9
+                stage_out[st_name].update({"cold_us": round(cold_ms[st_name] * 1e3, 2), "cold_GB_s": round(cold, 1),
+                                           "cold_frac_of_hbm_peak": round(cold / HBM_PEAK_GBS, 4)})
         else:
             peak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
             rate = amount / (ms * 1e-3) / 1e12
@@ -384,16 +390,24 @@ def main():
     dom = "ffn_gate_up"
     dkind, damount = work[dom]
     dms = dom_ms  # HIP events around the dominant kernel inside the timed steps
-    dpeak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
-    dach = damount / (dms * 1e-3) / 1e12
     # the record holds for the named workload only, not a share or another threshold
     traffic = (recorded_traffic(args.config)
                if share is None and args.theta is None and not args.fused_gather else None)
-    roofline = {"kernel": "grouped_gemm_dma_kernel<gated> (brownout_moe_ffn_gate_up)",
-                "bound": "mfma" if cfg.dtype == "bf16" else "alu",
-                "achieved": round(dach, 1), "peak": dpeak, "unit": "TFLOP/s",
-                "frac": round(dach / dpeak, 4), "traffic": traffic,
-                "per_launch": f"4*N*d*d_ff flop, N={N} rows; traffic: HBM bytes per launch (scaled pmc)"}
+    if skinny:
+        dach = damount / (dms * 1e-3) / 1e9
+        roofline = {"kernel": "skinny_gemm_kernel<gated> (brownout_moe_ffn_gate_up)", "bound": "hbm",
+                    "achieved": round(dach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(dach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "per_launch": f"weights 2*S*d*d_ff*s with S={S_w} segments with rows, plus N*d*s rows read and "
+                                  f"N*d_ff*s written, N={N}"}
+    else:
+        dpeak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
+        dach = damount / (dms * 1e-3) / 1e12
+        roofline = {"kernel": "grouped_gemm_dma_kernel<gated> (brownout_moe_ffn_gate_up)",
+                    "bound": "mfma" if cfg.dtype == "bf16" else "alu",
+                    "achieved": round(dach, 1), "peak": dpeak, "unit": "TFLOP/s",
+                    "frac": round(dach / dpeak, 4), "traffic": traffic,
+                    "per_launch": f"4*N*d*d_ff flop, N={N} rows; traffic: HBM bytes per launch (scaled pmc)"}
 
     result = {
         "metric": "grouped-MoE layer tokens/sec on 1 MI355X; FFN MFMA util %; route/permute HBM GB/s",

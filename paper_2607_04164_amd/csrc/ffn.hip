@@ -302,11 +302,11 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 // row read the row's contiguous bytes). The DMA and the barrier are issued
 // through inline asm: with the builtin, the compiler would wait for every
 // outstanding DMA before each LDS read and at each barrier, defeating the ring.
-// Per K-step: read the fragments of sub-step 1, run sub-step 0 on the MFMA
-// pipe, wait for this wave's DMAs of the next stage, barrier (after it every
-// wave has finished reading this stage and the next stage is resident), issue
-// the DMAs four stages ahead into this stage's slot, read the next stage's
-// sub-step-0 fragments, run sub-step 1.
+// Per K-step (four MFMA sub-steps of k = 16): fragments are read two
+// sub-steps ahead, so after sub-step 1 the stage's slot is no longer read; a
+// wait for this wave's copies of the next K-step and one barrier then release
+// the slot and make the next K-step resident, and sub-steps 2 and 3 issue the
+// copies of K-step kt+2 into the released slot, one per two MFMAs.
 
 // K-step and ring depth of the DMA kernels. BK = 64 makes every DMA row a
 // full 128-byte line (8 rows per instruction), which the L2 and MALL serve
@@ -427,25 +427,27 @@ __device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMA
             bf[mat][nb] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
 }
 
-// The MFMAs of one sub-step (A-fragment-major order) with the fragment reads
-// of the next sub-step spread between them, one read after every second
-// MFMA, in the order the next sub-step consumes them (all B fragments, then
-// A fragments), so that LDS returns do not arrive in one burst.
-template <class C>
-__device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                                 const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga)[C::MB],
-                                                 uint4 (&gb)[C::NMAT][C::NB], const char* stage, int wm, int wn,
-                                                 int lane, int kk) {
+// The MFMAs of one sub-step with the fragment reads of a later sub-step
+// (one read after every second MFMA, in the order that sub-step consumes
+// them: all B fragments, then A fragments) and, when DMA is set, half of the
+// wave's copies of a K-step (one after every other MFMA, DMA instructions
+// d0 .. d0 + NM/2 - 1).
+template <class C, bool DMA>
+__device__ __forceinline__ void mfmas_reads_dma(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                                const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga)[C::MB],
+                                                uint4 (&gb)[C::NMAT][C::NB], const char* stage, int wm, int wn,
+                                                int lane, int kk, const DmaSrc<C>& src, uint32_t dma_lds, int wave,
+                                                int kb, int d0) {
     constexpr int NM = C::NMAT * C::MB * C::NB, NR = C::MB + C::NMAT * C::NB;
-    static_assert(2 * NR == NM, "one read per two MFMAs");
+    static_assert(2 * NR == NM && C::DMA_PER_STAGE == NM, "one read and one copy per two MFMAs");
     const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
         const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
         acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        __builtin_amdgcn_sched_barrier(0);
         if (q & 1) {
             const int r = q >> 1;
-            __builtin_amdgcn_sched_barrier(0);
             if (r < C::NMAT * C::NB) {
                 const int rm = r / C::NB, rn = r % C::NB;
                 gb[rm][rn] = *(const uint4*)(stage + C::A_STAGE +
@@ -454,29 +456,9 @@ __device__ __forceinline__ void mfmas_with_reads(f32x16 (&acc)[C::NMAT][C::MB][C
                 const int ra = r - C::NMAT * C::NB;
                 ga[ra] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
             }
-            __builtin_amdgcn_sched_barrier(0);
+        } else if constexpr (DMA) {
+            dma_one<C>(src, dma_lds, wave, kb, d0 + (q >> 1));
         }
-    }
-}
-
-// The MFMAs of one sub-step with the wave's DMA instructions of a K-step
-// spread between them, so that a DMA issue that waits for queue space does
-// not hold back a run of MFMAs. DMA is a template argument: the K loop runs
-// as a main part that always copies and a two-step tail that never does, so
-// no copy sits behind a branch (a uniform branch per copy was 13x the
-// branches of a library GEMM of the same shape).
-template <class C, bool DMA>
-__device__ __forceinline__ void mfmas_with_dma(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                               const uint4 (&bf)[C::NMAT][C::NB], const DmaSrc<C>& src,
-                                               uint32_t stage_lds, int wave, int kb) {
-    constexpr int NM = C::NMAT * C::MB * C::NB;
-    static_assert(C::DMA_PER_STAGE == NM, "one DMA per MFMA");
-#pragma unroll
-    for (int q = 0; q < NM; ++q) {
-        const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
-        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (DMA) dma_one<C>(src, stage_lds, wave, kb, q);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -607,44 +589,44 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     if (after == kAfterNone && n > 1) wait_vmcnt<C::DMA_PER_STAGE>();
     else wait_vmcnt<0>();
     wg_barrier();
-    uint4 af0[C::MB], af1[C::MB];
-    uint4 bf0[C::NMAT][C::NB], bf1[C::NMAT][C::NB];
-    dma_frags<C>(af0, bf0, smem, wm, wn, lane, 0);
-
-    // The LDS reads of every K-step are unconditional (the last step reads a
-    // stale slot and drops it), so the compiler's LDS wait counts never merge
-    // two paths; only asm statements (DMA issue, DMA wait) sit behind branches.
-    // sched_barrier(0) fences keep each group of fragment reads ahead of the
-    // MFMA group that hides its latency.
+    // Fragments two sub-steps ahead, in four register sets (set j holds
+    // sub-step j of a K-step). Sub-step j reads sub-step j+2 (the next
+    // K-step's slot for j >= 2). After sub-step 1 every fragment of this
+    // K-step's slot is in registers: one barrier then releases the slot and
+    // (after this wave's wait) makes the next K-step's slot resident, and
+    // sub-steps 2 and 3 issue the copies of K-step kt+2 into the released
+    // slot, one per two MFMAs.
+    static_assert(C::SUB == 4, "four sub-steps per K-step");
+    uint4 af[4][C::MB];
+    uint4 bf[4][C::NMAT][C::NB];
+    dma_frags<C>(af[0], bf[0], smem, wm, wn, lane, 0);
+    dma_frags<C>(af[1], bf[1], smem, wm, wn, lane, 1);
     auto kstep = [&](int kt, auto with_dma) {
         constexpr bool DMA = decltype(with_dma)::value;
         const int slot = kt & 1;
-        const char* stage = smem + slot * C::STAGE;
-#pragma unroll
-        for (int j = 0; j < C::SUB; ++j) {
-            uint4(&fa)[C::MB] = (j & 1) ? af1 : af0;
-            uint4(&fb)[C::NMAT][C::NB] = (j & 1) ? bf1 : bf0;
-            uint4(&ga)[C::MB] = (j & 1) ? af0 : af1;
-            uint4(&gb)[C::NMAT][C::NB] = (j & 1) ? bf0 : bf1;
+        const uint32_t dma_lds = lds0 + slot * C::STAGE;
+        const int kb = (ka + kt + 2) * C::BK * 2;
+        auto sub = [&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            constexpr int jr = (j + 2) & 3;  // sub-step whose fragments this one reads
+            const char* rstage = smem + (j < 2 ? slot : slot ^ 1) * C::STAGE;
             __builtin_amdgcn_sched_barrier(0);
-            // the last sub-step carries the copies of K-step kt+2 (its slot was
-            // released by the barrier of the previous sub-step); the others
-            // carry the fragment reads of the next sub-step
-            if (j == C::SUB - 1)  // resolved by the unrolling
-                mfmas_with_dma<C, DMA>(acc, fa, fb, src, lds0 + slot * C::STAGE, wave, (ka + kt + 2) * C::BK * 2);
-            else
-                mfmas_with_reads<C>(acc, fa, fb, ga, gb, stage, wm, wn, lane, j + 1);
+            mfmas_reads_dma<C, DMA && (j >= 2)>(acc, af[j], bf[j], af[jr], bf[jr], rstage, wm, wn, lane, jr, src,
+                                                dma_lds, wave, kb, (j - 2) * (C::DMA_PER_STAGE / 2));
             __builtin_amdgcn_sched_barrier(0);
-            if (j == C::SUB - 2) {
-                // every copy issued so far (K-steps up to kt+1) must be resident
+            if constexpr (j == 1) {
+                // every copy issued so far (K-step kt+1) resident, every read
+                // of this slot done, in every wave
                 wait_vmcnt<0>();
                 lds_reads_done();
                 wg_barrier();
-                // registers of this sub-step are free now: next K-step, sub-step 0
-                dma_frags<C>(fa, fb, smem + (slot ^ 1) * C::STAGE, wm, wn, lane, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
-        }
+        };
+        sub(std::integral_constant<int, 0>{});
+        sub(std::integral_constant<int, 1>{});
+        sub(std::integral_constant<int, 2>{});
+        sub(std::integral_constant<int, 3>{});
     };
     int kt = 0;
     for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
