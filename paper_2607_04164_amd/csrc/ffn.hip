@@ -302,11 +302,12 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 // row read the row's contiguous bytes). The DMA and the barrier are issued
 // through inline asm: with the builtin, the compiler would wait for every
 // outstanding DMA before each LDS read and at each barrier, defeating the ring.
-// Per K-step (four MFMA sub-steps of k = 16): fragments are read two
-// sub-steps ahead, so after sub-step 1 the stage's slot is no longer read; a
-// wait for this wave's copies of the next K-step and one barrier then release
-// the slot and make the next K-step resident, and sub-steps 2 and 3 issue the
-// copies of K-step kt+2 into the released slot, one per two MFMAs.
+// Per K-step (four MFMA sub-steps of k = 16): by the end of sub-step 1
+// every fragment of the stage is in registers, and a barrier releases its
+// slot; sub-steps 2 and 3 issue the copies of K-step kt+2 into it, one per
+// two MFMAs; after sub-step 2 a wait for this wave's older copies and a
+// second barrier make K-step kt+1 resident, and sub-step 3 reads its first
+// fragments.
 
 // K-step and ring depth of the DMA kernels. BK = 64 makes every DMA row a
 // full 128-byte line (8 rows per instruction), which the L2 and MALL serve
@@ -427,37 +428,50 @@ __device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMA
             bf[mat][nb] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(mat * C::BN + wn * C::WTN + nb * 32 + l32, c));
 }
 
-// The MFMAs of one sub-step with the fragment reads of a later sub-step
-// (one read after every second MFMA, in the order that sub-step consumes
-// them: all B fragments, then A fragments) and, when DMA is set, half of the
-// wave's copies of a K-step (one after every other MFMA, DMA instructions
-// d0 .. d0 + NM/2 - 1).
-template <class C, bool DMA>
-__device__ __forceinline__ void mfmas_reads_dma(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
-                                                const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga)[C::MB],
-                                                uint4 (&gb)[C::NMAT][C::NB], const char* stage, int wm, int wn,
-                                                int lane, int kk, const DmaSrc<C>& src, uint32_t dma_lds, int wave,
-                                                int kb, int d0) {
+// Fragment read r of a sub-step (r < NMAT*NB: B fragments, then A).
+template <class C>
+__device__ __forceinline__ void frag_read(uint4 (&ga)[C::MB], uint4 (&gb)[C::NMAT][C::NB], const char* stage, int wm,
+                                          int wn, int l32, int c, int r) {
+    if (r < C::NMAT * C::NB) {
+        const int rm = r / C::NB, rn = r % C::NB;
+        gb[rm][rn] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
+    } else {
+        const int ra = r - C::NMAT * C::NB;
+        ga[ra] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
+    }
+}
+
+// The MFMAs of one sub-step with, between them, the fragment reads of RD
+// later sub-steps (RD = 1: one read after every second MFMA; RD = 2: one
+// after every MFMA, set 1 first) and, when DMA is set, half of the wave's
+// copies of a K-step (DMA instructions d0 .. d0 + NM/2 - 1), one after every
+// second MFMA. (Issuing the copies after each of the first NM/2 MFMAs
+// instead measured 1-3 % slower: spread copies are what the loop needs.)
+template <class C, int RD, bool DMA>
+__device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
+                                          const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga1)[C::MB],
+                                          uint4 (&gb1)[C::NMAT][C::NB], const char* st1, int kk1,
+                                          uint4 (&ga2)[C::MB], uint4 (&gb2)[C::NMAT][C::NB], const char* st2,
+                                          int kk2, int wm, int wn, int lane, const DmaSrc<C>& src,
+                                          uint32_t dma_lds, int wave, int kb, int d0) {
     constexpr int NM = C::NMAT * C::MB * C::NB, NR = C::MB + C::NMAT * C::NB;
     static_assert(2 * NR == NM && C::DMA_PER_STAGE == NM, "one read and one copy per two MFMAs");
-    const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
+    static_assert(!(RD == 2 && DMA), "at most one operation per MFMA");
+    const int l32 = lane & 31, c1 = kk1 * 2 + (lane >> 5), c2 = kk2 * 2 + (lane >> 5);
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
         const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
         acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
         __builtin_amdgcn_sched_barrier(0);
-        if (q & 1) {
-            const int r = q >> 1;
-            if (r < C::NMAT * C::NB) {
-                const int rm = r / C::NB, rn = r % C::NB;
-                gb[rm][rn] = *(const uint4*)(stage + C::A_STAGE +
-                                             lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
-            } else {
-                const int ra = r - C::NMAT * C::NB;
-                ga[ra] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
+        if constexpr (RD == 2) {
+            if (q < NR) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q);
+            else frag_read<C>(ga2, gb2, st2, wm, wn, l32, c2, q - NR);
+        } else {
+            if (q & 1) {
+                if constexpr (RD == 1) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q >> 1);
+            } else if constexpr (DMA) {
+                dma_one<C>(src, dma_lds, wave, kb, d0 + (q >> 1));
             }
-        } else if constexpr (DMA) {
-            dma_one<C>(src, dma_lds, wave, kb, d0 + (q >> 1));
         }
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -599,34 +613,40 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     static_assert(C::SUB == 4, "four sub-steps per K-step");
     uint4 af[4][C::MB];
     uint4 bf[4][C::NMAT][C::NB];
+    // Two barriers per K-step: after sub-step 1 the slot is released (its
+    // fragments are all in registers), after sub-step 2 the next K-step is
+    // resident (this wave waits only for copies older than the 8 it issued
+    // in sub-step 2). Sub-step 0 reads sub-steps 1 and 2, sub-step 1 reads
+    // sub-step 3, sub-step 3 reads the next K-step's sub-step 0.
     dma_frags<C>(af[0], bf[0], smem, wm, wn, lane, 0);
-    dma_frags<C>(af[1], bf[1], smem, wm, wn, lane, 1);
     auto kstep = [&](int kt, auto with_dma) {
         constexpr bool DMA = decltype(with_dma)::value;
         const int slot = kt & 1;
+        const char* cur = smem + slot * C::STAGE;
+        const char* nxt = smem + (slot ^ 1) * C::STAGE;
         const uint32_t dma_lds = lds0 + slot * C::STAGE;
         const int kb = (ka + kt + 2) * C::BK * 2;
-        auto sub = [&](auto jc) {
-            constexpr int j = decltype(jc)::value;
-            constexpr int jr = (j + 2) & 3;  // sub-step whose fragments this one reads
-            const char* rstage = smem + (j < 2 ? slot : slot ^ 1) * C::STAGE;
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas_reads_dma<C, DMA && (j >= 2)>(acc, af[j], bf[j], af[jr], bf[jr], rstage, wm, wn, lane, jr, src,
-                                                dma_lds, wave, kb, (j - 2) * (C::DMA_PER_STAGE / 2));
-            __builtin_amdgcn_sched_barrier(0);
-            if constexpr (j == 1) {
-                // every copy issued so far (K-step kt+1) resident, every read
-                // of this slot done, in every wave
-                wait_vmcnt<0>();
-                lds_reads_done();
-                wg_barrier();
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        };
-        sub(std::integral_constant<int, 0>{});
-        sub(std::integral_constant<int, 1>{});
-        sub(std::integral_constant<int, 2>{});
-        sub(std::integral_constant<int, 3>{});
+        constexpr int H = C::DMA_PER_STAGE / 2;
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas_ops<C, 2, false>(acc, af[0], bf[0], af[1], bf[1], cur, 1, af[2], bf[2], cur, 2, wm, wn, lane,
+                               src, dma_lds, wave, kb, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas_ops<C, 1, false>(acc, af[1], bf[1], af[3], bf[3], cur, 3, af[3], bf[3], cur, 3, wm, wn, lane,
+                               src, dma_lds, wave, kb, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        lds_reads_done();
+        wg_barrier();  // the slot is free
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas_ops<C, 0, DMA>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
+                             src, dma_lds, wave, kb, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DMA) wait_vmcnt<H>();
+        else wait_vmcnt<0>();
+        wg_barrier();  // the next K-step is resident
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas_ops<C, 1, DMA>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[0], bf[0], nxt, 0, wm, wn, lane,
+                             src, dma_lds, wave, kb, H);
+        __builtin_amdgcn_sched_barrier(0);
     };
     int kt = 0;
     for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
