@@ -263,6 +263,10 @@ LARGE_TILE_FFN = [
     ((0, 1290), 2048, 512, 192),
     ((1000, 0, 513, 1), 4096, 288, 352),   # not multiples of 64: register-staged 256-row kernels
     ((257,), 1024, 264, 200),
+    # one and two K-steps per tile (K = 64, 128): the K loops without a
+    # copying step, and stream-K pieces of a single K-step
+    ((1500, 700), 4096, 64, 128),
+    ((900, 300), 2048, 128, 64),
 ]
 
 
