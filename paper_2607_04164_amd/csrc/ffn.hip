@@ -302,12 +302,12 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 // row read the row's contiguous bytes). The DMA and the barrier are issued
 // through inline asm: with the builtin, the compiler would wait for every
 // outstanding DMA before each LDS read and at each barrier, defeating the ring.
-// Per K-step (four MFMA sub-steps of k = 16): by the end of sub-step 1
-// every fragment of the stage is in registers, and a barrier releases its
-// slot; sub-steps 2 and 3 issue the copies of K-step kt+2 into it, one per
-// two MFMAs; after sub-step 2 a wait for this wave's older copies and a
-// second barrier make K-step kt+1 resident, and sub-step 3 reads its first
-// fragments.
+// Per K-step (four MFMA sub-steps of k = 16): by the end of sub-step 0
+// every fragment of the stage is in registers (sub-steps 0 and 1 were read
+// during the previous K-step), and a barrier releases its slot; sub-steps
+// 1-3 issue the copies of K-step kt+2 into it (6, 5 and 5 per wave); after
+// sub-step 2 a wait for this wave's older copies and a second barrier make
+// K-step kt+1 resident, and sub-step 3 reads its first two sub-steps.
 
 // K-step and ring depth of the DMA kernels. BK = 64 makes every DMA row a
 // full 128-byte line (8 rows per instruction), which the L2 and MALL serve
@@ -443,11 +443,11 @@ __device__ __forceinline__ void frag_read(uint4 (&ga)[C::MB], uint4 (&gb)[C::NMA
 
 // The MFMAs of one sub-step with, between them, the fragment reads of RD
 // later sub-steps (RD = 1: one read after every second MFMA; RD = 2: one
-// after every MFMA, set 1 first) and, when DMA is set, half of the wave's
-// copies of a K-step (DMA instructions d0 .. d0 + NM/2 - 1), one after every
-// second MFMA. (Issuing the copies after each of the first NM/2 MFMAs
-// instead measured 1-3 % slower: spread copies are what the loop needs.)
-template <class C, int RD, bool DMA>
+// after every MFMA, set 1 first) and ND of the wave's copies of a K-step
+// (DMA instructions d0 .. d0 + ND - 1), one after every (NM / ND)-th MFMA.
+// (Issuing a sub-step's copies after each of its first MFMAs instead
+// measured 1-3 % slower: the copies must be spread.)
+template <class C, int RD, int ND>
 __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
                                           const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga1)[C::MB],
                                           uint4 (&gb1)[C::NMAT][C::NB], const char* st1, int kk1,
@@ -456,7 +456,8 @@ __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
                                           uint32_t dma_lds, int wave, int kb, int d0) {
     constexpr int NM = C::NMAT * C::MB * C::NB, NR = C::MB + C::NMAT * C::NB;
     static_assert(2 * NR == NM && C::DMA_PER_STAGE == NM, "one read and one copy per two MFMAs");
-    static_assert(!(RD == 2 && DMA), "at most one operation per MFMA");
+    static_assert(ND >= 0 && ND <= NM / 2, "at most one copy per two MFMAs");
+    constexpr int STEP = ND > 0 ? NM / ND : NM;
     const int l32 = lane & 31, c1 = kk1 * 2 + (lane >> 5), c2 = kk2 * 2 + (lane >> 5);
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
@@ -466,12 +467,11 @@ __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
         if constexpr (RD == 2) {
             if (q < NR) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q);
             else frag_read<C>(ga2, gb2, st2, wm, wn, l32, c2, q - NR);
-        } else {
-            if (q & 1) {
-                if constexpr (RD == 1) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q >> 1);
-            } else if constexpr (DMA) {
-                dma_one<C>(src, dma_lds, wave, kb, d0 + (q >> 1));
-            }
+        } else if constexpr (RD == 1) {
+            if (q & 1) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q >> 1);
+        }
+        if constexpr (ND > 0) {
+            if (q % STEP == 0 && q / STEP < ND) dma_one<C>(src, dma_lds, wave, kb, d0 + q / STEP);
         }
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -613,12 +613,12 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     static_assert(C::SUB == 4, "four sub-steps per K-step");
     uint4 af[4][C::MB];
     uint4 bf[4][C::NMAT][C::NB];
-    // Two barriers per K-step: after sub-step 1 the slot is released (its
-    // fragments are all in registers), after sub-step 2 the next K-step is
-    // resident (this wave waits only for copies older than the 8 it issued
-    // in sub-step 2). Sub-step 0 reads sub-steps 1 and 2, sub-step 1 reads
-    // sub-step 3, sub-step 3 reads the next K-step's sub-step 0.
+    // Sub-step 0 reads sub-steps 2 and 3, so a barrier after it releases the
+    // slot; sub-steps 1-3 issue the copies of K-step kt+2 (6, 5, 5); after
+    // sub-step 2 a wait for this wave's older copies and a second barrier
+    // make K-step kt+1 resident; sub-step 3 reads its sub-steps 0 and 1.
     dma_frags<C>(af[0], bf[0], smem, wm, wn, lane, 0);
+    dma_frags<C>(af[1], bf[1], smem, wm, wn, lane, 1);
     auto kstep = [&](int kt, auto with_dma) {
         constexpr bool DMA = decltype(with_dma)::value;
         const int slot = kt & 1;
@@ -626,26 +626,26 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
         const char* nxt = smem + (slot ^ 1) * C::STAGE;
         const uint32_t dma_lds = lds0 + slot * C::STAGE;
         const int kb = (ka + kt + 2) * C::BK * 2;
-        constexpr int H = C::DMA_PER_STAGE / 2;
+        constexpr int D1 = 6, D2 = 5, D3 = C::DMA_PER_STAGE - D1 - D2;
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, false>(acc, af[0], bf[0], af[1], bf[1], cur, 1, af[2], bf[2], cur, 2, wm, wn, lane,
-                               src, dma_lds, wave, kb, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 1, false>(acc, af[1], bf[1], af[3], bf[3], cur, 3, af[3], bf[3], cur, 3, wm, wn, lane,
-                               src, dma_lds, wave, kb, 0);
+        mfmas_ops<C, 2, 0>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
+                           dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
         lds_reads_done();
         wg_barrier();  // the slot is free
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 0, DMA>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
-                             src, dma_lds, wave, kb, 0);
+        mfmas_ops<C, 0, DMA ? D1 : 0>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
+                                      src, dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (DMA) wait_vmcnt<H>();
+        mfmas_ops<C, 0, DMA ? D2 : 0>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
+                                      src, dma_lds, wave, kb, D1);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DMA) wait_vmcnt<D1 + D2>();
         else wait_vmcnt<0>();
         wg_barrier();  // the next K-step is resident
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 1, DMA>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[0], bf[0], nxt, 0, wm, wn, lane,
-                             src, dma_lds, wave, kb, H);
+        mfmas_ops<C, 2, DMA ? D3 : 0>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
+                                      src, dma_lds, wave, kb, D1 + D2);
         __builtin_amdgcn_sched_barrier(0);
     };
     int kt = 0;
