@@ -186,12 +186,174 @@ __global__ __launch_bounds__(kSkThreads, 1) void skinny_gemm_kernel(SkinnyParams
     }
 }
 
+// ---- the same FFN with every operand copied straight into LDS (K % 64 == 0)
+//
+// The register-staged kernel above keeps about two chunks of weights in
+// flight per wave, and its activation stores wait for loads issued one
+// chunk earlier, so each chunk waits for most of a memory latency. Here the
+// activation rows and the workgroup's weight rows of a 64-column chunk are
+// copied with global_load_lds (one 128-byte line per row and copy row, 1 KB
+// per instruction) into a ring of slots, NSL-1 chunks ahead, and both MFMA
+// operands are read from LDS. A slot row's 16-byte pieces are XOR-swizzled by
+// (row & 7), so the 8 rows of a read group fall on different banks. One
+// barrier per chunk: after it every wave's copies of the chunk have landed
+// and every wave has finished reading the slot the next copies overwrite.
+// Decode-shaped (8 segments, d = 2048, d_ff = 1408): gate/up 26 -> 21 us,
+// down 14.0 -> 13.5 us. Reading the next chunk's fragments during the
+// current chunk's MFMAs measured slower; what bounds the kernel now is
+// likelier the access pattern (each weight row is read 128 bytes at a time,
+// K/64 visits per row) than the per-chunk steps.
+constexpr int kS2KC = 64;             // K columns per chunk
+constexpr int kS2RowB = kS2KC * 2;    // bytes per slot row (one 128-byte line)
+
+template <int NMAT>
+struct S2Cfg {
+    static constexpr int ROWS = kSkRows + NMAT * kSkCols;  // activation rows, then each matrix's weight rows
+    static constexpr int SLOT = ROWS * kS2RowB;            // 16 KB (down) / 24 KB (gate/up)
+    static constexpr int NSL = NMAT == 2 ? 6 : 8;            // 144 KB / 128 KB of LDS
+    static constexpr int NDMA = ROWS / 8;                    // copy instructions per chunk
+    static constexpr int DPW = NDMA / 4;                     // per wave
+    static_assert(NDMA % 4 == 0 && kSkRows % 64 == 0 && kSkCols % 64 == 0, "copy rows split evenly");
+    static_assert(NSL - 2 <= 7, "run-time copy wait covers at most 7 later chunks");
+    static_assert(NSL * SLOT <= 160 * 1024, "LDS of one workgroup");
+};
+
+__device__ __forceinline__ int s2_off(int row, int chunk) { return row * kS2RowB + ((chunk ^ (row & 7)) << 4); }
+
+template <bool GATED>
+__global__ __launch_bounds__(kSkThreads, 1) void skinny_dma_kernel(SkinnyParams p) {
+    constexpr int NMAT = GATED ? 2 : 1;
+    using C = S2Cfg<NMAT>;
+    __shared__ __align__(16) char lds[C::NSL * C::SLOT];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int ncb = ceil_div(p.N, kSkCols);
+    const int s = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+    if (s >= p.n_seg) return;
+    const int beg = min(max(p.offsets[s], 0), p.rows_cap);
+    const int end = min(max(p.offsets[s + 1], beg), p.rows_cap);
+    if (end <= beg) return;
+    const int K = p.K, N = p.N;
+    const int nch = K / kS2KC;
+    const int n0 = cb * kSkCols;
+    const int r16 = lane & 15, q = lane >> 4;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+
+    // copy instruction i of this wave fills slot rows [8g, 8g+8), g = wave*DPW + i:
+    // rows [0, 64) are activation rows, then 64 weight rows of each matrix
+    const char* base[C::DPW];
+    uint32_t off[C::DPW];
+    int lane_v = lane;
+    asm volatile("" : "+v"(lane_v));  // keep the per-lane parts from being hoisted and spilled
+    const int lrow = lane_v >> 3, lchk = lane_v & 7;
+#pragma unroll
+    for (int i = 0; i < C::DPW; ++i) {
+        const int g = wave * C::DPW + i;
+        const int region = g >> 3;  // 0: activations, 1 + mat: weights of matrix mat
+        const int row = 8 * g + lrow;
+        if (region > 0) {
+            const uint16_t* w = (GATED && region == 2) ? p.B1 : p.B0;
+            base[i] = (const char*)(w + ((size_t)s * N + n0) * K);
+            const int wr = min(n0 + (row - 64 * region), N - 1) - n0;
+            off[i] = (uint32_t)((size_t)wr * K * 2 + ((lchk ^ (row & 7)) << 4));
+        } else {
+            base[i] = (const char*)p.A;
+            off[i] = 0;  // set per pass
+        }
+    }
+    auto issue = [&](int c) {
+        const uint32_t slot = lds0 + (uint32_t)((c % C::NSL) * C::SLOT);
+#pragma unroll
+        for (int i = 0; i < C::DPW; ++i)
+            dma16s(base[i] + (size_t)c * kS2RowB, off[i], slot + (uint32_t)((wave * C::DPW + i) * 1024));
+    };
+
+    for (int m0 = beg; m0 < end; m0 += kSkRows) {
+        // source rows of the pass: [m0, m0+64) clamped to the segment, gathered when A is
+#pragma unroll
+        for (int i = 0; i < C::DPW; ++i) {
+            const int g = wave * C::DPW + i;
+            if ((g >> 3) == 0) {
+                const int row = 8 * g + lrow;
+                const int arow = gathered_row(p.a_rows, p.a_count, min(m0 + row, end - 1));
+                off[i] = (uint32_t)((size_t)arow * K * 2 + ((lchk ^ (row & 7)) << 4));
+            }
+        }
+        f32x4 acc[NMAT][4];
+#pragma unroll
+        for (int mat = 0; mat < NMAT; ++mat)
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) acc[mat][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < C::NSL - 1 && c < nch; ++c) issue(c);
+        for (int c = 0; c < nch; ++c) {
+            // this wave's copies of chunk c are done when at most the later
+            // chunks' copies are outstanding; after the barrier every wave's
+            // are, and no wave still reads the slot of chunk c-1
+            wait_vmcnt_rt<C::DPW>(min(C::NSL - 2, nch - 1 - c));
+            lds_reads_done();
+            wg_barrier();
+            if (c + C::NSL - 1 < nch) issue(c + C::NSL - 1);
+            const char* sl = lds + (c % C::NSL) * C::SLOT;
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                v4u wv[NMAT], xv[4];
+#pragma unroll
+                for (int mat = 0; mat < NMAT; ++mat) {
+                    const int row = kSkRows + mat * kSkCols + wave * 16 + r16;
+                    wv[mat] = *(const v4u*)(sl + s2_off(row, kk * 4 + q));
+                }
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) xv[nt] = *(const v4u*)(sl + s2_off(nt * 16 + r16, kk * 4 + q));
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                    for (int mat = 0; mat < NMAT; ++mat)
+                        acc[mat][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv[mat]),
+                                                                               __builtin_bit_cast(bf16x8, xv[nt]),
+                                                                               acc[mat][nt], 0, 0, 0);
+            }
+        }
+
+        // epilogue: lane holds D[weight row 4q+i][segment row r16] of every
+        // row tile nt, i.e. output columns col .. col+3 of row m0+16nt+r16
+        const int col = n0 + wave * 16 + 4 * q;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int row = m0 + nt * 16 + r16;
+            if (row >= end) continue;
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if constexpr (GATED) v[i] = silu_mul(acc[0][nt][i], acc[NMAT - 1][nt][i]);
+                else v[i] = acc[0][nt][i];
+            }
+            uint16_t* dst = p.C + (size_t)row * N + col;
+            if (col + 3 < N) {
+                *(uint2*)dst = make_uint2(pack_bf16x2_hw(v[0], v[1]), pack_bf16x2_hw(v[2], v[3]));
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (col + i < N) dst[i] = f32_to_bf16(v[i]);
+            }
+        }
+        // the ring is refilled by the next pass: every read done, and the
+        // stores complete before its copies are counted
+        wait_vmcnt<0>();
+        lds_reads_done();
+        wg_barrier();
+    }
+}
+
 template <bool GATED>
 hipError_t launch_skinny(const SkinnyParams& sp, hipStream_t s) {
     const int64_t blocks = (int64_t)sp.n_seg * ceil_div(sp.N, kSkCols);
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((skinny_gemm_kernel<GATED>), dim3((unsigned)blocks), dim3(kSkThreads), 0, s, sp);
+    // the copies address A rows by 32-bit byte offsets from A
+    const int64_t a_rows = sp.a_rows ? sp.a_count : sp.rows_cap;
+    if (sp.K % kS2KC == 0 && a_rows * sp.K * 2 < ((int64_t)1 << 31) && (int64_t)kSkCols * sp.K * 2 < ((int64_t)1 << 31))
+        hipLaunchKernelGGL((skinny_dma_kernel<GATED>), dim3((unsigned)blocks), dim3(kSkThreads), 0, s, sp);
+    else
+        hipLaunchKernelGGL((skinny_gemm_kernel<GATED>), dim3((unsigned)blocks), dim3(kSkThreads), 0, s, sp);
     return hipGetLastError();
 }
 

@@ -232,6 +232,10 @@ SKINNY_FFN = [
     ((9, 14, 55, 59, 45, 32, 27, 62), 81, 2048, 1408),  # decode-shaped layer (G=8, top-6 of 64 tokens)
     ((3, 0, 70, 1), 2, 328, 136),     # K tails (328 = 256 + 72, 136), N tails (136 = 2*64 + 8), two passes
     ((64, 65, 1, 0, 120), 0, 264, 72),  # exact and ragged 64-row passes, 72 = 64 + 8 columns
+    # K multiples of 64 select the all-copy kernels: fewer chunks than ring
+    # slots (K = 64, 192, 320), N tails, two passes, empty segments
+    ((3, 0, 70, 1), 2, 320, 192),
+    ((64, 65, 1, 0, 120), 0, 136, 64),
 ]
 
 
