@@ -1,6 +1,10 @@
 // Skinny grouped GEMMs for decode-sized batches: the per-united-expert
 // SwiGLU FFN of Sec. 2.1 when every group holds only a few dozen rows, so the
-// layer is bound by streaming the united-expert weights, not by MFMA.
+// layer is bound by streaming the united-expert weights, not by MFMA. Two
+// kernels share the grid and the MFMA layout: skinny_dma_kernel (further
+// down) copies every operand straight into LDS and runs whenever K is a
+// multiple of 64; skinny_gemm_kernel, described here, stages operands through
+// registers and takes any K.
 //
 // One workgroup (4 waves) owns one segment and 64 output columns; wave w owns
 // columns n0 .. n0+15 with n0 = 64*cb + 16*w (for the fused gate/up GEMM: those
