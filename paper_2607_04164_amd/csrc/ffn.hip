@@ -333,7 +333,7 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 #ifdef BMOE_FORCE_GROUP_M
 constexpr int kGroupM = BMOE_FORCE_GROUP_M;
 #else
-constexpr int kGroupM = 4;
+constexpr int kGroupM = 8;
 #endif
 constexpr int kDmaBK = 64;
 constexpr int kSkPartBytes = 256 * 256 * 4;  // fp32 accumulators of one tile piece
