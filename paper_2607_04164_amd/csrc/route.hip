@@ -788,10 +788,11 @@ hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
 template <int TB>
 hipError_t launch_bf16(const RouteArgs& a, hipStream_t s) {
     // two 64-column units per wave and copy step where two ring slots still
-    // fit (fewer barriers per byte); the decode-sized tile of 16 tokens with
-    // up to 64 experts keeps one
+    // fit (fewer barriers per byte); tiles of 16 or 32 tokens with up to 64
+    // experts keep one (32 tokens: five 24 KB slots instead of two 48 KB
+    // ones, measured 4 % faster warm and 8 % cold on 8192 tokens)
     if (a.E <= 16) return launch_one<MODE_BF16, TB, 1, 2>(a, s);
-    if constexpr (TB > 1) {
+    if constexpr (TB > 2) {
         if (a.E <= 64) return launch_one<MODE_BF16, TB, 4, 2>(a, s);
     } else {
         if (a.E <= 64) return launch_one<MODE_BF16, TB, 4, 1>(a, s);
