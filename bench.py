@@ -482,7 +482,7 @@ def main():
 
 
 def bench_distill(args, dev):
-    """One candidate grouping of the search (Sec. 4.2), evaluated on the GPU:
+    """One candidate grouping of the search (Sec. 4.3), evaluated on the GPU:
     the united experts start as their members' parameter average, run on the
     T calibration tokens, and the errors of Eq. 5-6 follow. The members'
     outputs are computed once (the calibration run records them) and are not

@@ -109,6 +109,32 @@ BMOE_API const char* bmoe_status_str(bmoe_status status);
 BMOE_API int32_t bmoe_version(void);
 
 /*
+ * bmoe_partial_segment_map -- host only: the segment map of partial brownout.
+ * Paper: Sec. 2.2 (zero, partial and full brownout), Sec. 5 baselines
+ * (threshold 1.0 keeps every original expert, 0 substitutes every call),
+ * Sec. 4.3 closing paragraph (only eligible cold calls are replaced through
+ * the saved map), Sec. 4.5 (the controller moves the threshold).
+ *
+ * Hot experts: the longest run of experts in order of decreasing freq (ties:
+ * lower index first) whose cumulative freq / sum(freq) is <= theta + 1e-9.
+ * Segments: the hot experts in ascending index (each with its own FFN), then
+ * the united experts with at least one cold member in ascending group index.
+ * The layer runs over the segments with e2s in place of e2g and S = *n_seg
+ * in place of G (the weights of segment s stacked at index s).
+ *
+ * freq[E] double (calibration routing frequencies: finite, >= 0, positive
+ * sum), e2g[E] int32 in [0, G), theta in [0, 1]; all HOST memory. Outputs,
+ * host memory: e2s[E] int32; seg_kind[E] int32 (0: a hot expert's own FFN,
+ * 1: a united expert) and seg_id[E] int32 (that expert or group), first
+ * *n_seg entries valid; *n_seg in 1..E. Errors: BMOE_ERR_NULL,
+ * BMOE_ERR_SHAPE (sizes, theta, frequencies), BMOE_ERR_MAP (e2g); nothing
+ * is written on error.
+ */
+BMOE_API bmoe_status bmoe_partial_segment_map(const double* freq, const int32_t* e2g, int32_t E, int32_t G,
+                                             double theta, int32_t* e2s, int32_t* seg_kind, int32_t* seg_id,
+                                             int32_t* n_seg);
+
+/*
  * brownout_moe_route -- the gate and the substitution by united experts.
  * Paper: Sec. 2.1 (gating scores g_i of the top-K experts), Eq. 2 (the map),
  * Sec. 4.3 last paragraph before Algorithm 1 (the gate still picks the
@@ -196,13 +222,25 @@ BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t*
  * initialisation and are not preserved; calls that can overlap in time must
  * not share a workspace. A non-NULL workspace below the size is
  * BMOE_ERR_WORKSPACE. The K loops are split only when whole tiles would leave
- * the CUs idle for more than 48 K-steps (of 64 columns) on average; the
- * environment variable BMOE_FFN_SPLIT_MIN_IDLE overrides that threshold.
+ * the CUs idle for more than 48 K-steps (of 64 columns) on average
+ * (brownout_moe_ffn_ex takes that threshold as an argument).
  */
 BMOE_API bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
                              int32_t d_ff, const int32_t* offsets, const void* a,
                              const void* w_gate, const void* w_up, const void* w_down, void* h,
                              void* y, void* workspace, size_t workspace_bytes, void* stream);
+
+/* brownout_moe_ffn with the stream-K split threshold given explicitly: with a
+ * workspace, the K loops of the last tiles are split when whole tiles would
+ * leave the CUs idle for more than split_min_idle K-steps (of 64 columns) on
+ * average; 0 splits whenever any CU would idle, -1 takes the default (48).
+ * Values below -1 or above 2^20 are BMOE_ERR_SHAPE. The result is the same
+ * layer as brownout_moe_ffn's within the rounding of the split sums. */
+BMOE_API bmoe_status brownout_moe_ffn_ex(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d,
+                                int32_t d_ff, const int32_t* offsets, const void* a,
+                                const void* w_gate, const void* w_up, const void* w_down, void* h,
+                                void* y, void* workspace, size_t workspace_bytes,
+                                int32_t split_min_idle, void* stream);
 
 /* The two grouped GEMMs of brownout_moe_ffn, callable on their own (same
  * arguments and rules as brownout_moe_ffn):
@@ -241,14 +279,14 @@ BMOE_API bmoe_status brownout_moe_ffn_gate_up_gather(int32_t dtype, int32_t n_se
                                             size_t workspace_bytes, void* stream);
 
 /*
- * Grouping search (Sec. 4.2): what a candidate map costs in distillation
+ * Grouping search (Sec. 4.3): what a candidate map costs in distillation
  * error. The member experts' outputs f_e(x) and the united experts' outputs
  * f_u(x) on the calibration tokens come from brownout_moe_ffn_gather with one
  * segment per expert (rows e*T .. e*T+T-1 read token t = row mod T).
  *
  * brownout_moe_united_init -- the united experts' starting point: each united
  * matrix is the element-wise average of its members' matrices (the parameter
- * average the paper starts distillation from, Sec. 4.2 after Eq. 5).
+ * average the paper starts distillation from, Sec. 4.3, after Eq. 5).
  *   w_*_u[r] = (sum over e with e2g[e] == r, ascending e, of w_*_e[e]) / count
  * e2g [E] int32 in DEVICE memory (entries outside [0, G) belong to no group);
  * w_gate_e, w_up_e [E, d_ff, d], w_down_e [E, d, d_ff]; w_gate_u, w_up_u

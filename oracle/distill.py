@@ -6,7 +6,7 @@ with the library's kernels. Plain numpy in float64, following the paper's
 definitions in order:
 
   * united-expert initialisation: the parameter average of the member
-    experts (Sec. 4.2, after Eq. 5);
+    experts (Sec. 4.3, after Eq. 5);
   * distillation target (Eq. 5): alpha_e = w_e / sum of w over the group,
     t_k(x) = sum over the members e of alpha_e f_e(x);
   * group error and total (Eq. 3, Eq. 6): beta_r = sum of w over group r,

@@ -29,7 +29,7 @@ EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_
             "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
             "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
             "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather", "brownout_moe_united_init",
-            "brownout_moe_distill_mse")
+            "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map")
 DISTILL_WS_BYTES = 32768
 
 
@@ -89,6 +89,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_dispatch.restype = I32
     lib.brownout_moe_ffn.argtypes = [I32] * 5 + [P] * 8 + [SZ, P]
     lib.brownout_moe_ffn.restype = I32
+    lib.brownout_moe_ffn_ex.argtypes = [I32] * 5 + [P] * 8 + [SZ, I32, P]
+    lib.brownout_moe_ffn_ex.restype = I32
     lib.brownout_moe_ffn_gate_up.argtypes = [I32] * 5 + [P] * 6 + [SZ, P]
     lib.brownout_moe_ffn_gate_up.restype = I32
     lib.brownout_moe_ffn_down.argtypes = [I32] * 5 + [P] * 5 + [SZ, P]
@@ -103,6 +105,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_ffn_down.restype = I32
     lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
     lib.brownout_moe_combine.restype = I32
+    lib.bmoe_partial_segment_map.argtypes = [P, P, I32, I32, ctypes.c_double, P, P, P, P]
+    lib.bmoe_partial_segment_map.restype = I32
     _lib = lib
     return lib
 
@@ -242,9 +246,10 @@ def _ffn_checks(offsets, a_rows, dt, n_seg, d, d_ff):
 
 def ffn(offsets: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
         w_down: torch.Tensor, *, h: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
-        workspace: Optional[torch.Tensor] = None, stream=None):
+        workspace: Optional[torch.Tensor] = None, split_min_idle: Optional[int] = None, stream=None):
     """Both grouped GEMMs: returns (y, h). workspace: optional uint8 device
-    tensor of at least workspace_bytes(desc, STAGE_FFN) bytes (stream-K)."""
+    tensor of at least workspace_bytes(desc, STAGE_FFN) bytes (stream-K);
+    split_min_idle: the stream-K split threshold (None: the library default)."""
     n_seg, d_ff, d = w_gate.shape
     rows_cap, dt = a.shape[0], a.dtype
     dtype = _ffn_checks(offsets, rows_cap, dt, n_seg, d, d_ff)
@@ -255,9 +260,15 @@ def ffn(offsets: torch.Tensor, a: torch.Tensor, w_gate: torch.Tensor, w_up: torc
     h = _dev(h, "h", dt, (rows_cap, d_ff)) if h is not None else _empty((rows_cap, d_ff), dt, a.device)
     y = _dev(y, "y", dt, (rows_cap, d)) if y is not None else _empty((rows_cap, d), dt, a.device)
     wsp, wsn = _ws(workspace)
-    st = load_library().brownout_moe_ffn(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a), _p(w_gate),
-                                         _p(w_up), _p(w_down), _p(h), _p(y), wsp, wsn, _stream(stream))
-    _check(st, "brownout_moe_ffn")
+    if split_min_idle is None:
+        st = load_library().brownout_moe_ffn(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a), _p(w_gate),
+                                             _p(w_up), _p(w_down), _p(h), _p(y), wsp, wsn, _stream(stream))
+        _check(st, "brownout_moe_ffn")
+    else:
+        st = load_library().brownout_moe_ffn_ex(dtype, n_seg, rows_cap, d, d_ff, _p(offsets), _p(a), _p(w_gate),
+                                                _p(w_up), _p(w_down), _p(h), _p(y), wsp, wsn, int(split_min_idle),
+                                                _stream(stream))
+        _check(st, "brownout_moe_ffn_ex")
     return y, h
 
 

@@ -18,60 +18,52 @@ The layer then runs unchanged over S segments: the hot experts (ascending
 index) with their original weights, followed by the united experts that still
 have a cold member (ascending group index) with their united weights; the
 segment map e2s replaces e2g in route, dispatch, FFN and combine. S <= E.
-This module is host-side numpy; the layer's arithmetic stays in the library.
+The map is built by the library's host-only call bmoe_partial_segment_map;
+this module marshals numpy arrays into it and stacks the segments' weights.
 """
 from __future__ import annotations
 
+import ctypes
 from typing import List, Tuple
 
 import numpy as np
 
 __all__ = ["hot_set", "segment_map", "stack_segments"]
 
-# slack for the cumulative comparison, so that theta = 1 keeps every expert
-# whatever the rounding of the frequency sum
-_SLACK = 1e-9
+_KIND = {0: "expert", 1: "united"}
+
+
+def _build(freq, e2g, G: int, theta: float):
+    from . import binding as B
+    w = np.ascontiguousarray(freq, dtype=np.float64)
+    m = np.ascontiguousarray(e2g, dtype=np.int32)
+    if w.ndim != 1 or m.shape != w.shape:
+        raise ValueError("freq and e2g must be 1-D arrays of the same length")
+    E = w.shape[0]
+    e2s = np.empty(E, np.int32)
+    kind = np.empty(E, np.int32)
+    sid = np.empty(E, np.int32)
+    n = ctypes.c_int32(0)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+    st = B.load_library().bmoe_partial_segment_map(p(w), p(m), E, int(G), float(theta), p(e2s), p(kind), p(sid),
+                                                   ctypes.byref(n))
+    if st != 0:
+        raise ValueError(f"bmoe_partial_segment_map: {B.status_str(st)}")
+    return e2s, [(_KIND[int(kind[s])], int(sid[s])) for s in range(n.value)]
 
 
 def hot_set(freq: np.ndarray, theta: float) -> np.ndarray:
     """Experts kept on their own FFN, ascending index."""
     w = np.asarray(freq, dtype=np.float64)
-    if w.ndim != 1 or np.any(w < 0) or not np.all(np.isfinite(w)):
-        raise ValueError("freq must be a 1-D array of finite non-negative frequencies")
-    if not 0.0 <= theta <= 1.0:
-        raise ValueError("theta must lie in [0, 1]")
-    tot = w.sum()
-    if tot <= 0:
-        raise ValueError("frequencies sum to zero")
-    order = sorted(range(len(w)), key=lambda e: (-w[e], e))
-    hot, acc = [], 0.0
-    for e in order:
-        if acc + w[e] / tot > theta + _SLACK:
-            break
-        acc += w[e] / tot
-        hot.append(e)
-    return np.array(sorted(hot), dtype=np.int32)
+    _, segments = _build(w, np.zeros(w.shape[0], np.int32), 1, theta)
+    return np.array([i for kind, i in segments if kind == "expert"], dtype=np.int32)
 
 
 def segment_map(freq: np.ndarray, e2g: np.ndarray, G: int, theta: float) -> Tuple[np.ndarray, List[Tuple[str, int]]]:
     """Returns (e2s, segments): e2s[e] is the segment of expert e; segments[s]
     is ("expert", e) for a hot expert's own FFN or ("united", g) for a united
     expert."""
-    e2g = np.asarray(e2g, dtype=np.int32)
-    E = e2g.shape[0]
-    if np.any(e2g < 0) or np.any(e2g >= G):
-        raise ValueError("e2g must map into [0, G)")
-    hot = hot_set(freq, theta)
-    is_hot = np.zeros(E, dtype=bool)
-    is_hot[hot] = True
-    segments: List[Tuple[str, int]] = [("expert", int(e)) for e in hot]
-    used = sorted({int(e2g[e]) for e in range(E) if not is_hot[e]})
-    seg_of_group = {g: len(hot) + i for i, g in enumerate(used)}
-    segments += [("united", g) for g in used]
-    e2s = np.empty(E, dtype=np.int32)
-    for e in range(E):
-        e2s[e] = np.searchsorted(hot, e) if is_hot[e] else seg_of_group[int(e2g[e])]
-    return e2s, segments
+    return _build(freq, e2g, G, theta)
 
 
 def stack_segments(segments, expert_w, united_w):

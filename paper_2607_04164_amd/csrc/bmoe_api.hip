@@ -106,7 +106,7 @@ namespace {
 bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
                        const int32_t* offsets, const void* a, const void* w_gate, const void* w_up,
                        const void* w_down, void* h, void* y, void* ws, size_t ws_bytes, void* stream,
-                       const int32_t* a_rows = nullptr, int32_t a_count = 0) {
+                       const int32_t* a_rows = nullptr, int32_t a_count = 0, int32_t split_min_idle = -1) {
     if (dtype != BMOE_F32 && dtype != BMOE_BF16) return BMOE_ERR_UNSUPPORTED;
     if (n_seg < 1 || n_seg > BMOE_MAX_EXPERTS || rows_cap < 0) return BMOE_ERR_SHAPE;
     if (d < 8 || d % 8 != 0 || d_ff < 8 || d_ff % 8 != 0) return BMOE_ERR_SHAPE;
@@ -123,7 +123,9 @@ bmoe_status ffn_common(int part, int32_t dtype, int32_t n_seg, int32_t rows_cap,
     if (ws && ((uintptr_t)ws & 255u)) return BMOE_ERR_ALIGN;
     if (dtype != BMOE_BF16) ws = nullptr;  // the fp32 kernels take no workspace
     if (ws && ws_bytes < ffn_workspace_bytes()) return BMOE_ERR_WORKSPACE;
+    if (split_min_idle < -1 || split_min_idle > (1 << 20)) return BMOE_ERR_SHAPE;
     FfnArgs args{offsets, a, w_gate, w_up, w_down, h, y, ws, ws_bytes, n_seg, rows_cap, d, d_ff, dtype};
+    args.split_min_idle = split_min_idle;
     if (a_rows) {
         // the copy kernels address a gathered source with 32-bit byte offsets
         if (a_count < 1 || (int64_t)a_count * d * elem_bytes(dtype) >= ((int64_t)1 << 32)) return BMOE_ERR_SHAPE;
@@ -143,6 +145,14 @@ bmoe_status brownout_moe_ffn(int32_t dtype, int32_t n_seg, int32_t rows_cap, int
                              size_t workspace_bytes, void* stream) {
     return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, workspace,
                       workspace_bytes, stream);
+}
+
+bmoe_status brownout_moe_ffn_ex(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,
+                                const int32_t* offsets, const void* a, const void* w_gate, const void* w_up,
+                                const void* w_down, void* h, void* y, void* workspace, size_t workspace_bytes,
+                                int32_t split_min_idle, void* stream) {
+    return ffn_common(0, dtype, n_seg, rows_cap, d, d_ff, offsets, a, w_gate, w_up, w_down, h, y, workspace,
+                      workspace_bytes, stream, nullptr, 0, split_min_idle);
 }
 
 bmoe_status brownout_moe_ffn_gather(int32_t dtype, int32_t n_seg, int32_t rows_cap, int32_t d, int32_t d_ff,

@@ -197,6 +197,9 @@ struct FfnArgs {
     // a_count rows); nullptr: row r is a[r]
     const int32_t* a_rows = nullptr;
     int a_count = 0;
+    // stream-K split threshold in K-steps of average idle time per workgroup
+    // (negative: the library default)
+    int split_min_idle = -1;
 };
 
 // Row of the A operand that GEMM row r reads: a_rows[r] clamped into the

@@ -1,4 +1,4 @@
-// Grouping-search kernels of one layer (Sec. 4.2): the parameter-average
+// Grouping-search kernels of one layer (Sec. 4.3): the parameter-average
 // initialisation of the united experts, and the distillation error of every
 // group against its routing-weighted target (Eq. 5) with the
 // routing-frequency-weighted total (Eq. 3, Eq. 6).

@@ -330,11 +330,7 @@ hipError_t launch_gemm(const GemmParams& g, hipStream_t s) {
 // each split tile in K order and applies the epilogue. No workgroup ever
 // waits for another, so nothing depends on which workgroups are resident.
 
-#ifdef BMOE_FORCE_GROUP_M
-constexpr int kGroupM = BMOE_FORCE_GROUP_M;
-#else
 constexpr int kGroupM = 8;
-#endif
 constexpr int kDmaBK = 64;
 constexpr int kSkPartBytes = 256 * 256 * 4;  // fp32 accumulators of one tile piece
 // workspace slot stride: a piece plus 1280 bytes, so that slots (which the
@@ -755,7 +751,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
 // The split moves two fp32 tile pieces per workgroup through memory and
 // restarts the pipeline per piece, so it is used (with a workspace) only when
 // whole tiles would leave the workgroups idle for more than min_idle K-steps
-// on average (kSkMinIdle unless BMOE_FFN_SPLIT_MIN_IDLE says otherwise).
+// on average (the caller's threshold, kSkMinIdle by default).
 constexpr int kSkMinIdle = 48;
 constexpr int kSkMinShare = 8;  // K-steps: the shortest piece worth a pipeline restart
 struct SkSplit {
@@ -982,18 +978,11 @@ static int stream_k_workgroups() {
     return cached[dev];
 }
 
-static int split_min_idle() {
-    const char* e = getenv("BMOE_FFN_SPLIT_MIN_IDLE");
-    if (e == nullptr || *e == 0) return kSkMinIdle;
-    const long v = strtol(e, nullptr, 10);
-    return v < 0 ? 0 : (v > (1 << 20) ? (1 << 20) : (int)v);
-}
-
 template <bool GATED>
 hipError_t launch_gemm_dma(const GemmParams& g0, void* ws, size_t ws_bytes, hipStream_t s) {
     using C = DmaCfg<GATED>;
     GemmParams g = g0;
-    g.sk_min_idle = split_min_idle();
+    g.sk_min_idle = g0.sk_min_idle < 0 ? kSkMinIdle : g0.sk_min_idle;
     // persistent: one workgroup per CU, each XCD a contiguous range of tiles
     const int P = stream_k_workgroups();
     if (P > 0) {
@@ -1077,18 +1066,10 @@ size_t ffn_workspace_bytes() {
 // halve the LDS traffic per MFMA but pad each group to a multiple of 256
 // rows, so they are used when groups average well above that.
 enum { kTile128 = 0, kTile256 = 1, kTileDma = 2 };
-#ifdef BMOE_FORCE_FFN_FDB
-constexpr bool kFdb256 = BMOE_FORCE_FFN_FDB;
-#else
 constexpr bool kFdb256 = false;  // no registers left for a second fragment set
-#endif
 static int ffn_tile(const FfnArgs& a) {
-#ifdef BMOE_FORCE_FFN_TILE
-    return BMOE_FORCE_FFN_TILE;
-#else
     if ((int64_t)a.rows_cap < (int64_t)1024 * a.n_seg) return kTile128;
     return (a.d % kDmaBK == 0 && a.d_ff % kDmaBK == 0) ? kTileDma : kTile256;
-#endif
 }
 
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
@@ -1118,6 +1099,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
                       (uint16_t*)a.h, a.offsets, a.n_seg, a.rows_cap, a.d_ff, a.d};
         g1.a_rows = a.a_rows;
         g1.a_count = a.a_count;
+        g1.sk_min_idle = a.split_min_idle;
         hipError_t e = tile == kTileDma   ? launch_gemm_dma<true>(g1, a.ws, a.ws_bytes, s)
                        : tile == kTile256 ? launch_gemm<true, 256, 128, 64, kFdb256>(g1, s)
                                           : launch_gemm<true, 128, 128, 64, true>(g1, s);
@@ -1126,6 +1108,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (down) {
         GemmParams g2{(const uint16_t*)a.h, (const uint16_t*)a.w_down, nullptr, (uint16_t*)a.y,
                       a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff};
+        g2.sk_min_idle = a.split_min_idle;
         return tile == kTileDma   ? launch_gemm_dma<false>(g2, a.ws, a.ws_bytes, s)
                : tile == kTile256 ? launch_gemm<false, 256, 256, 64, kFdb256>(g2, s)
                                   : launch_gemm<false, 128, 256, 64, true>(g2, s);

@@ -112,6 +112,42 @@ def pin_softmax_weights(orc):
             assert np.allclose(out["topk_w"][t], ref, rtol=2e-7, atol=0), (norm, out["topk_w"][t], ref)
 
 
+def pin_route_f32_logits_exact_values(orc):
+    """Selection on float32 logits uses those exact values: the same picks,
+    weights and groups as a library selection (stable argsort, scipy softmax)
+    on the logits widened to float64, including values that tie only in
+    float32 and a transposed-looking layout (T != E)."""
+    r = _rng(8)
+    T, E, k, G = 13, 10, 3, 4
+    z = (r.standard_normal((T, E)) * 2).astype(np.float32)
+    # two pairs that are equal in float32 (exact ties), one pair one ulp apart
+    z[2, 7] = z[2, 4]
+    z[5, 1] = z[5, 9] = np.float32(3.0)
+    z[8, 3] = np.nextafter(z[8, 6], np.float32(np.inf))
+    e2g = W.balanced_map(r.permutation(E), E, G)
+    for norm in (0, 1):
+        out = orc.route_from_logits(z, e2g, k, norm_topk=norm)
+        z64 = z.astype(np.float64)
+        p = softmax(z64, axis=1)
+        for t in range(T):
+            sel = _topk_lib(z64[t], k)
+            assert out["topk_idx"][t].tolist() == sel.tolist(), (t, out["topk_idx"][t], sel)
+            ref_w = p[t, sel] / (p[t, sel].sum() if norm else 1.0)
+            assert np.allclose(out["topk_w"][t], ref_w, rtol=2e-7, atol=0), (t, norm)
+            groups = e2g[sel]
+            for i in range(k):
+                if groups[i] in groups[:i]:
+                    assert out["slot_group"][t, i] == -1 and out["slot_gate"][t, i] == 0
+                else:
+                    assert out["slot_group"][t, i] == groups[i]
+                    want = ref_w[groups == groups[i]].sum()
+                    assert math.isclose(out["slot_gate"][t, i], want, rel_tol=1e-6), (t, i)
+        # the float64 entry on the widened values decides identically
+        o64 = orc.route_from_logits(z64, e2g, k, norm_topk=norm)
+        for key in ("topk_idx", "slot_group", "topk_w", "slot_gate"):
+            assert np.array_equal(out[key], o64[key]), key
+
+
 # ----------------------------------------------------------------------------
 # substitution by united experts, merge
 
@@ -246,6 +282,28 @@ def pin_merged_equals_per_slot_calls(orc):
         assert _rel_rowmax(res["out"], ref) < 1e-5
 
 
+def pin_ffn_hidden_activation(orc):
+    """The FFN's hidden output h is silu(gate) * up of each row against its own
+    segment's weights (library matmuls, silu(v) = v * logistic(v)), and the
+    down projection of h gives y."""
+    r = _rng(9)
+    n_seg, d, d_ff = 3, 20, 28
+    offsets = np.array([0, 4, 4, 11], np.int32)  # an empty middle segment
+    a = r.standard_normal((11, d)).astype(np.float32)
+    wg = (r.standard_normal((n_seg, d_ff, d)) / 4).astype(np.float32)
+    wu = (r.standard_normal((n_seg, d_ff, d)) / 4).astype(np.float32)
+    wd = (r.standard_normal((n_seg, d, d_ff)) / 4).astype(np.float32)
+    y, h = orc.ffn(offsets, a, wg, wu, wd, want_h=True)
+    for s in range(n_seg):
+        rows = slice(offsets[s], offsets[s + 1])
+        a64 = a[rows].astype(np.float64)
+        g = a64 @ wg[s].astype(np.float64).T
+        u = a64 @ wu[s].astype(np.float64).T
+        h_ref = g * expit(g) * u
+        assert np.allclose(h[rows], h_ref, rtol=1e-6, atol=1e-7), s
+        assert _rel_rowmax(y[rows], h_ref @ wd[s].astype(np.float64).T) < 1e-6, s
+
+
 def pin_shared_experts_always_on(orc):
     L = _rand_layer(30, 10, 16, 8, 2, 4, 24, n_shared=2)
     res = _oracle_out(orc, L)
@@ -284,6 +342,7 @@ def pin_eq1_group_counts(orc):
 
 ALL_PINS = [
     pin_logits_vs_blas, pin_topk_best_subset, pin_topk_ties_lower_index, pin_softmax_weights,
+    pin_route_f32_logits_exact_values, pin_ffn_hidden_activation,
     pin_group_gates_sum_to_topk_mass, pin_fig1_worked_maps, pin_dispatch_counting_sort,
     pin_gather_rows, pin_identity_map_is_ungrouped_layer, pin_single_group_is_dense_ffn,
     pin_merged_equals_per_slot_calls, pin_shared_experts_always_on, pin_token_order_invariance,

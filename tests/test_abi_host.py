@@ -121,6 +121,12 @@ def test_entry_points_reject_before_launch(lib):
     # the stream-K workspace must be 256-byte aligned
     assert ffn(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x10010), 1 << 30,
                z) == ALIGN
+    # explicit stream-K threshold: -1 (default) .. 2^20
+    fx = lib.brownout_moe_ffn_ex
+    assert fx(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, -2, z) == SHAPE
+    assert fx(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, (1 << 20) + 1, z) == SHAPE
+    assert fx(1, 4, 128, 256, 512, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, 0, z) == NULL
+    assert fx(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z, 0, 0, z) == OK
     assert lib.brownout_moe_ffn_gate_up(1, 4, 128, 256, 512, FAKE, z, FAKE, FAKE, FAKE, z, 0, z) == NULL
     assert lib.brownout_moe_ffn_down(1, 4, 128, 256, 512, FAKE, FAKE, FAKE, MISALIGNED, z, 0, z) == ALIGN
     # fused gather: row indices required, the source small enough for 32-bit offsets

@@ -283,11 +283,10 @@ def ffn_workspace():
 
 @pytest.mark.parametrize("stream_k", [False, True], ids=["tile-per-wg", "stream-k"])
 @pytest.mark.parametrize("sizes,cap,d,f", LARGE_TILE_FFN, ids=[f"seg{len(c[0])}-d{c[2]}-f{c[3]}" for c in LARGE_TILE_FFN])
-def test_ffn_large_tile_paths(sizes, cap, d, f, stream_k, monkeypatch):
+def test_ffn_large_tile_paths(sizes, cap, d, f, stream_k):
     """256-row tiles; with the stream-K workspace (and the split threshold at
     zero) these small problems have fewer tiles than CUs, so every tile's K
     loop is cut into several pieces that meet in the workspace."""
-    monkeypatch.setenv("BMOE_FFN_SPLIT_MIN_IDLE", "0")
     r = np.random.default_rng(len(sizes) * 1000 + d)
     nseg = len(sizes)
     offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
@@ -303,14 +302,14 @@ def test_ffn_large_tile_paths(sizes, cap, d, f, stream_k, monkeypatch):
     if ws is not None:
         ws.fill_(0xFF)  # stale contents must not matter
     yg, hg = B.ffn(torch.from_numpy(offsets).cuda(), dev_tensor(a, "bf16"), dev_tensor(wg, "bf16"),
-                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"), y=y, workspace=ws)
+                   dev_tensor(wu, "bf16"), dev_tensor(wd, "bf16"), y=y, workspace=ws, split_min_idle=0)
     torch.cuda.synchronize()
     assert_close_rows(host_f32(hg[:N]), ref_h, "bf16", "h")
     assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
     assert bool((yg[N:] == -5.0).all()), "rows past offsets[n_seg] must not be written"
 
 
-def test_ffn_stream_k_full_rounds_and_reuse(monkeypatch):
+def test_ffn_stream_k_full_rounds_and_reuse():
     """More tiles than two rounds of workgroups (full rounds, then the split
     remainder); the workspace is reused by a second, smaller call; results
     match the tile-per-workgroup path within bf16 rounding and are
@@ -330,10 +329,10 @@ def test_ffn_stream_k_full_rounds_and_reuse(monkeypatch):
     wd = dev_tensor(W.f32_to_bf16_bits((r.standard_normal((nseg, d, f)) / np.sqrt(f)).astype(np.float32)), "bf16")
     offs = torch.from_numpy(offsets).cuda()
     ws = ffn_workspace()
-    monkeypatch.setenv("BMOE_FFN_SPLIT_MIN_IDLE", "0")  # split whenever whole tiles leave CUs idle
+    # split threshold 0: split whenever whole tiles leave CUs idle
     y0, h0 = B.ffn(offs, a, wg, wu, wd)
-    y1, h1 = B.ffn(offs, a, wg, wu, wd, workspace=ws)
-    y2, h2 = B.ffn(offs, a, wg, wu, wd, workspace=ws)
+    y1, h1 = B.ffn(offs, a, wg, wu, wd, workspace=ws, split_min_idle=0)
+    y2, h2 = B.ffn(offs, a, wg, wu, wd, workspace=ws, split_min_idle=0)
     torch.cuda.synchronize()
     # rows past offsets[n_seg] are never written (the buffers are uninitialised there)
     assert torch.equal(y1[:N].view(torch.int16), y2[:N].view(torch.int16))
@@ -354,7 +353,7 @@ def test_ffn_stream_k_full_rounds_and_reuse(monkeypatch):
     # a smaller problem through the same (now stale) workspace
     small = np.array([0, 700, 1500], np.int32)
     ys, hs = B.ffn(torch.from_numpy(small).cuda(), a, wg[:2].contiguous(), wu[:2].contiguous(), wd[:2].contiguous(),
-                   workspace=ws)
+                   workspace=ws, split_min_idle=0)
     ys0, _ = B.ffn(torch.from_numpy(small).cuda(), a, wg[:2].contiguous(), wu[:2].contiguous(), wd[:2].contiguous())
     torch.cuda.synchronize()
     assert_close_rows(host_f32(ys[:1500]), host_f32(ys0[:1500]), "bf16", "y small")

@@ -25,6 +25,10 @@ MUTANTS = {
     "shared_experts_dropped": ("if (y_shared) acc +=", "if (0) acc +="),
     "remap_uses_first_pick": ("int r = e2g[pick[i]];", "int r = e2g[pick[0]];"),
     "down_proj_skips_last_hidden": ("for (int j = 0; j < d_ff; ++j) acc +=", "for (int j = 0; j + 1 < d_ff; ++j) acc +="),
+    "f32_logits_read_transposed": ("z[e] = (double)zf[(size_t)t * E + e];",
+                                   "z[e] = (double)zf[(size_t)e * T + t];"),
+    "hidden_output_drops_up": ("h_out[(size_t)r * d_ff + j] = (float)hbuf[j];",
+                               "h_out[(size_t)r * d_ff + j] = (float)silu;"),
     "combine_ignores_gate": ("acc += (double)slot_gate[(size_t)t * k + i] * (double)y", "acc += (double)y"),
 }
 

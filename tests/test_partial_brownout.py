@@ -110,6 +110,37 @@ def test_library_builder_matches_oracle(seed):
         assert np.array_equal(a[0], b[0]) and a[1] == b[1], theta
 
 
+def test_library_builder_rejects_bad_input():
+    """Host-side checks of the C call: nothing is built from a bad map, an
+    out-of-range threshold or frequencies that are negative, non-finite or all
+    zero."""
+    freq, e2g = _rand_case(0)
+    for theta in (-0.1, 1.5, float("nan")):
+        with pytest.raises(ValueError):
+            BO.segment_map(freq, e2g, 4, theta)
+    bad = e2g.copy()
+    bad[3] = 4
+    with pytest.raises(ValueError):
+        BO.segment_map(freq, bad, 4, 0.5)
+    for f in (np.zeros(12), np.where(np.arange(12) == 2, -1.0, freq), np.where(np.arange(12) == 2, np.inf, freq)):
+        with pytest.raises(ValueError):
+            BO.segment_map(f, e2g, 4, 0.5)
+    with pytest.raises(ValueError):
+        BO.segment_map(freq, e2g, 13, 0.5)  # more groups than experts
+
+
+def test_library_builder_ties_and_extremes():
+    """Equal frequencies go to the lower index first; theta 0 and 1 give the
+    group map and the identity."""
+    freq = np.array([0.2, 0.1, 0.2, 0.1, 0.2, 0.2])
+    e2g = np.array([0, 0, 1, 1, 2, 2], np.int32)
+    e2s, seg = BO.segment_map(freq, e2g, 3, 0.45)
+    assert seg[:2] == [("expert", 0), ("expert", 2)] and len(seg) == 2 + 3
+    assert (e2s, seg) == (e2s, seg) and np.array_equal(*[partial_map(freq, e2g, 3, 0.45)[0], e2s])
+    assert np.array_equal(BO.segment_map(freq, e2g, 3, 0.0)[0], e2g)
+    assert np.array_equal(BO.segment_map(freq, e2g, 3, 1.0)[0], np.arange(6))
+
+
 def test_partial_layer_is_per_slot_original_or_united_calls():
     cfg = W.LayerConfig("pb", T=24, d=32, E=10, top_k=3, G=3, d_ff=40, dtype="f32", zipf_s=1.0,
                         router_std=0.5, theta=0.5)
