@@ -93,3 +93,45 @@ def group_boundary_tokens(perm_token: np.ndarray, offsets: np.ndarray) -> np.nda
         if offsets[r + 1] > offsets[r]:
             out += [perm_token[offsets[r]], perm_token[offsets[r + 1] - 1]]
     return np.unique(np.array(out, dtype=np.int64))
+
+
+def stream_k_split_rows(offsets, n_cols, K, gated: bool, n_cu: int, split_min_idle: int = 48):
+    """Rows of every output tile whose K loop the persistent 256-row GEMM
+    splits across workgroups (stream-K) when it runs with the FFN workspace.
+
+    This restates the kernel's tile schedule only to choose which rows a
+    parity test samples (a mistake here weakens the sample, it cannot make a
+    wrong result pass): segments in order, inside a segment groups of 8
+    M-tiles of 256 rows with the N-tiles outer; P = the CU count rounded down
+    to a multiple of 8 workgroups; whole rounds of one tile per workgroup,
+    and the K-steps (64 columns each) of the tiles after them split evenly
+    when whole tiles would leave the workgroups idle for more than
+    split_min_idle K-steps on average (only the last partial round when that
+    gives every workgroup at least 8 K-steps, else the last one to two)."""
+    BM, BN, BK, GM = 256, (128 if gated else 256), 64, 8
+    P = n_cu // 8 * 8
+    offs = [int(o) for o in offsets]
+    n_seg = len(offs) - 1
+    mts = [-(-(offs[s + 1] - offs[s]) // BM) for s in range(n_seg)]
+    NT = -(-n_cols // BN)
+    total = sum(mts) * NT
+    nk = K // BK
+    if P == 0 or total == 0 or K % BK:
+        return np.zeros(0, np.int64)
+    rounds = -(-total // P)
+    if (rounds * P - total) * nk <= split_min_idle * P:
+        return np.zeros(0, np.int64)
+    full = total // P
+    rest = (total - full * P) * nk
+    F = full if rest >= 8 * P else max(0, full - 1)
+    first_mt = np.concatenate([[0], np.cumsum(mts)])
+    rows = set()
+    for L in range(F * P, total):
+        s = int(np.searchsorted(first_mt * NT, L, side="right") - 1)
+        local = L - first_mt[s] * NT
+        mg = local // (GM * NT)
+        gm = min(GM, mts[s] - mg * GM)
+        mt = mg * GM + (local - mg * GM * NT) % gm
+        r0 = offs[s] + mt * BM
+        rows.update(range(r0, min(r0 + BM, offs[s + 1])))
+    return np.array(sorted(rows), np.int64)

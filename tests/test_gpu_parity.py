@@ -19,7 +19,7 @@ import torch
 import oracle
 from oracle.partial import partial_map
 from gpu_util import (TOL, assert_close_rows, assert_gates, desc_of, dev_tensor, device_weights,
-                      group_boundary_tokens, host_f32, to_storage)
+                      group_boundary_tokens, host_f32, stream_k_split_rows, to_storage)
 from paper_2607_04164_amd import binding as B
 from paper_2607_04164_amd import brownout as BO
 from paper_2607_04164_amd import workload as W
@@ -626,14 +626,23 @@ def test_partial_brownout_layer(theta):
     check_layer(PL, ref, layer, out)
 
 
-@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral", "partial", "mixtral-tp8"])
-def test_full_size_sampled(name):
-    """Full-size workloads; mixtral-tp8 is rank 3's share of the Mixtral-shaped
-    layer under 8-way tensor parallelism (d_ff 1792)."""
-    L = W.tp_share(full_case("mixtral"), 8, 3) if name == "mixtral-tp8" else full_case(name)
+FULL_FLOAT_SAMPLE = {"mixtral": 1024, "heavy": 1024}  # tokens whose float outputs are checked
+
+
+def _sample_tokens(cfg, dsp, n_random, seed):
+    """Group-boundary tokens (first and last row of every segment), the first
+    and last token, and n_random further tokens drawn without replacement."""
+    rng = np.random.default_rng(seed)
+    base = np.concatenate([group_boundary_tokens(dsp["perm_token"], dsp["offsets"]), [0, cfg.T - 1]])
+    rest = np.setdiff1d(np.arange(cfg.T), base)
+    extra = rng.choice(rest, size=min(n_random, rest.size), replace=False)
+    return np.unique(np.concatenate([base, extra])).astype(np.int64)
+
+
+def _check_full_size(L, layer, out, n_random, seed):
+    """Integer outputs in full; float outputs (layer output and the united
+    experts' rows) on a token sample against the oracle run on those tokens."""
     cfg = L.cfg
-    layer, out = run_layer(L)
-    # integer outputs in full
     r = oracle.route(L.f32("x"), L.f32("w_router"), L.bias, L.e2g, cfg.top_k, cfg.norm_topk)
     dsp = oracle.dispatch(r["slot_group"], cfg.G)
     gr, gd = layer.bufs["route"], layer.bufs["dispatch"]
@@ -643,12 +652,7 @@ def test_full_size_sampled(name):
     for k in ("counts", "offsets", "slot_row"):
         assert np.array_equal(gd[k].cpu().numpy(), dsp[k]), k
     assert np.array_equal(gd["perm_token"][:dsp["N"]].cpu().numpy(), dsp["perm_token"])
-    # float outputs on a token sample: group boundary rows plus random tokens
-    rng = np.random.default_rng(1)
-    extra = 8 if name == "mixtral" else 32
-    sample = np.unique(np.concatenate([group_boundary_tokens(dsp["perm_token"], dsp["offsets"]),
-                                       rng.choice(cfg.T, size=min(extra, cfg.T), replace=False),
-                                       [0, cfg.T - 1]]))
+    sample = _sample_tokens(cfg, dsp, n_random, seed)
     sub = dataclasses.replace(L, cfg=cfg.with_(T=len(sample)), x=L.x[sample].copy())
     ref = oracle.layer(sub, want_intermediates=True)
     assert np.array_equal(ref["topk_idx"], r["topk_idx"][sample])
@@ -659,3 +663,60 @@ def test_full_size_sampled(name):
     ref_rows = ref["slot_row"][sr >= 0]
     assert_close_rows(host_f32(layer.bufs["y"][torch.from_numpy(rows).long().cuda()]),
                       ref["y"][ref_rows], cfg.dtype, "y_perm")
+    return r, dsp, sample
+
+
+def _check_split_tiles(L, layer, dsp):
+    """Every row of every output tile whose K loop the GEMMs split across
+    workgroups (the stream-K pieces summed by the fixup kernel): h and y
+    against the oracle's FFN on those rows."""
+    cfg = L.cfg
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    offs = dsp["offsets"]
+    rows_h = stream_k_split_rows(offs, cfg.d_ff, cfg.d, True, n_cu)
+    rows_y = stream_k_split_rows(offs, cfg.d, cfg.d_ff, False, n_cu)
+    rows = np.union1d(rows_h, rows_y).astype(np.int64)
+    if rows.size == 0:
+        return 0
+    seg = np.searchsorted(offs, rows, side="right") - 1
+    x = L.f32("x")
+    wg, wu, wd = L.f32("w_gate"), L.f32("w_up"), L.f32("w_down")
+    for s in np.unique(seg):
+        rs = rows[seg == s]
+        a = x[dsp["perm_token"][rs]]
+        y_ref, h_ref = oracle.ffn(np.array([0, len(rs)], np.int32), a, wg[s:s + 1], wu[s:s + 1], wd[s:s + 1],
+                                  want_h=True)
+        idx = torch.from_numpy(rs).cuda()
+        assert_close_rows(host_f32(layer.bufs["h"][idx]), h_ref, cfg.dtype, f"h split rows (segment {s})")
+        assert_close_rows(host_f32(layer.bufs["y"][idx]), y_ref, cfg.dtype, f"y split rows (segment {s})")
+    return rows.size
+
+
+@pytest.mark.parametrize("name", ["decode", "fine", "heavy", "mixtral", "partial", "mixtral-tp8"])
+def test_full_size_sampled(name):
+    """Full-size workloads, seed 0, through LayerForward (the FFN with its
+    stream-K workspace, as the benchmark runs it); mixtral-tp8 is rank 3's
+    share of the Mixtral-shaped layer under 8-way tensor parallelism (d_ff
+    1792). Integers in full; the float outputs of at least 1024 tokens at the
+    Mixtral and heavy shapes (all of decode's 64), and every row of the tiles
+    the GEMMs split."""
+    L = W.tp_share(full_case("mixtral"), 8, 3) if name == "mixtral-tp8" else full_case(name)
+    cfg = L.cfg
+    layer, out = run_layer(L)
+    _, dsp, sample = _check_full_size(L, layer, out, FULL_FLOAT_SAMPLE.get(name, 48), seed=1)
+    if name in FULL_FLOAT_SAMPLE:
+        assert len(sample) >= FULL_FLOAT_SAMPLE[name]
+    n_split = _check_split_tiles(L, layer, dsp)
+    if name == "mixtral":
+        # the down GEMM's last partial round is split at this shape
+        assert n_split > 0
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("name", ["tiny", "decode", "fine", "heavy", "mixtral"])
+def test_full_size_more_seeds(name, seed):
+    """The five workloads at full size with seeds 1 and 2: every integer
+    output in full, the float outputs on a sample of tokens."""
+    L = W.make_layer(W.CONFIGS[name], seed)
+    layer, out = run_layer(L)
+    _check_full_size(L, layer, out, 32, seed=seed)
