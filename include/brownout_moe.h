@@ -187,7 +187,11 @@ BMOE_API bmoe_status brownout_moe_route(const bmoe_desc* desc, const void* x, co
  * workspace: bmoe_workspace_bytes(desc, BMOE_STAGE_DISPATCH) bytes, 256-byte
  * aligned, ALL ZERO before the first call that uses it; every call leaves it
  * all zero again when it completes on the stream. Two calls that share a
- * workspace must not overlap in time.
+ * workspace must not overlap in time. A call that finds the workspace not
+ * zero (for example after an earlier call on it was cut short) writes the
+ * "no rows" result instead: counts all 0, offsets[0..G-1] = 0 and
+ * offsets[G] = -1 (the sentinel to check), every slot_row -1, no row copied;
+ * the FFN and combine then see no rows. It still leaves the workspace zero.
  * Implementation: a histogram with LDS atomics and a single-pass decoupled
  * look-back scan across token tiles, then a 128-bit row gather.
  */

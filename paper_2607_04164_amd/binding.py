@@ -30,6 +30,7 @@ EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_
             "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
             "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather", "brownout_moe_united_init",
             "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map")
+STATUS_CODES = {v: k for k, v in STATUS.items()}
 DISTILL_WS_BYTES = 32768
 
 

@@ -16,6 +16,8 @@
 // Kernel 2 (permute), one wave per token: adds offsets[group] to the relative
 // row, writes perm_token, and copies x[t] into each of its rows with 128-bit
 // loads and stores. Workgroup 0 clears the look-back state for the next call.
+#include <algorithm>
+
 #include "bmoe_common.h"
 #include "stream_io.h"
 
@@ -27,11 +29,22 @@ constexpr uint32_t kFlagAgg = 1u, kFlagPrefix = 2u;
 // Upper bound on polls of one predecessor's status word. Predecessors publish
 // without waiting, so the bound is only reached if the workspace was not
 // zeroed before the first call; the walk then gives up instead of hanging.
-constexpr int kMaxPolls = 1 << 22;
+constexpr int kMaxPolls = 1 << 20;
 
+// Workspace: the tile ticket, the call's error word and one status word per
+// (tile, group). A clean call finds ticket 0, so its tiles draw tickets
+// 0 .. ntiles-1 and tile 0 clears the error word. A ticket at or past ntiles
+// (the workspace was not zero) or a look-back that gives up sets the error
+// word; the permute kernel then writes the "no rows" result (counts 0,
+// offsets 0 with offsets[G] = -1, every slot_row -1) and nothing else, and
+// its last workgroup to finish (counted in `done`) clears the error word. The
+// permute kernel's workgroup 0 clears the ticket and the status words, so the
+// next call starts clean either way.
 struct DispatchWs {
     int32_t ticket;
-    int32_t pad[63];
+    int32_t err;
+    int32_t done;
+    int32_t pad[61];
     // followed by uint64_t status[ntiles * G]
 };
 
@@ -60,7 +73,12 @@ __global__ __launch_bounds__(kTile) void hist_scan_kernel(const int32_t* __restr
     }
     __syncthreads();
     const int tile = s_tile;
-    if (tile >= ntiles) return;  // workspace not zeroed: no out-of-range writes
+    if (tile >= ntiles) {
+        // the workspace was not zero: no out-of-range writes, the call reports it
+        if (tid == 0) __hip_atomic_store(&hdr->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    if (tile == 0 && tid == 0) __hip_atomic_store(&hdr->err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int t = tile * kTile + tid;
     const bool tok = t < T;
 
@@ -130,7 +148,10 @@ __global__ __launch_bounds__(kTile) void hist_scan_kernel(const int32_t* __restr
                 else j0 -= lpg;
             }
             if (__ballot(wait) != 0ull) {
-                if (++polls > kMaxPolls) break;  // workspace was not zeroed
+                if (++polls > kMaxPolls) {  // workspace was not zeroed: the call reports it
+                    if (lane == 0) __hip_atomic_store(&hdr->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
                 __builtin_amdgcn_s_sleep(1);
             }
         }
@@ -174,25 +195,65 @@ __global__ __launch_bounds__(kTile) void hist_scan_kernel(const int32_t* __restr
     }
 }
 
+// First step of both permute kernels. Workgroup 0 leaves the look-back state
+// (ticket and status words) all zero for the next call; nothing in this
+// kernel reads it. When the histogram kernel reported an error, the call's
+// result is "no rows": workgroup 0 writes counts 0 and offsets 0 with
+// offsets[G] = -1, every thread sets its n_slots slots (from slot index o0)
+// to -1, and the kernel stops (returns true).
+__device__ __forceinline__ bool permute_prologue(void* ws, int32_t* slot_row, int32_t* counts, int32_t* offsets,
+                                                 int T, int k, int G, int ntiles, int64_t o0, int n_slots) {
+    DispatchWs* hdr = (DispatchWs*)ws;
+    const int tid = threadIdx.x;
+    const int err = __hip_atomic_load(&hdr->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (blockIdx.x == 0) {
+        uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
+        const int n = ntiles * G;
+        for (int i = tid; i < n; i += 256) status[i] = 0ull;
+        if (tid == 0) hdr->ticket = 0;
+        if (err) {
+            for (int g = tid; g <= G; g += 256) {
+                if (g < G) counts[g] = 0;
+                offsets[g] = g < G ? 0 : -1;
+            }
+        }
+    }
+    if (!err) return false;
+    for (int i = 0; i < n_slots; ++i)
+        if (o0 + i < (int64_t)T * k) slot_row[o0 + i] = -1;
+    // every workgroup has read the error word (err is the same for all of
+    // them: nothing clears it before the last one is counted)
+    __syncthreads();
+    if (tid == 0) {
+        __threadfence();
+        if (atomicAdd(&hdr->done, 1) == (int)gridDim.x - 1) {
+            __hip_atomic_store(&hdr->err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&hdr->done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    return true;
+}
+
+// Clears a dispatch workspace of `bytes` bytes (a multiple of 8).
+__global__ __launch_bounds__(256) void ws_clear_kernel(uint64_t* ws, int64_t n_words) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_words; i += (int64_t)gridDim.x * 256)
+        ws[i] = 0ull;
+}
+
 // One wave per token. VEC: 16-byte chunks each lane moves per batch.
 template <int VEC>
 __global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict__ slot_group,
                                                       int32_t* __restrict__ slot_row,
-                                                      const int32_t* __restrict__ offsets,
+                                                      int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ offsets,
                                                       int32_t* __restrict__ perm_token,
                                                       const uint4* __restrict__ x,
                                                       uint4* __restrict__ x_perm, void* ws, int T,
                                                       int k, int G, int nch, int ntiles, int rows_cap) {
     const int tid = threadIdx.x, lane = tid & 63;
-    if (blockIdx.x == 0) {
-        // leave the look-back state all zero for the next call
-        DispatchWs* hdr = (DispatchWs*)ws;
-        uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
-        const int n = ntiles * G;
-        for (int i = tid; i < n; i += 256) status[i] = 0ull;
-        if (tid == 0) hdr->ticket = 0;
-    }
     const int t = blockIdx.x * 4 + (tid >> 6);
+    if (permute_prologue(ws, slot_row, counts, offsets, T, k, G, ntiles, (int64_t)t * k + lane, lane < k ? 1 : 0))
+        return;
     if (t >= T) return;
     int row = -1;
     if (lane < k) {
@@ -234,19 +295,13 @@ __global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict_
 // from x itself): one thread per slot writes its row and the row's token.
 __global__ __launch_bounds__(256) void permute_index_kernel(const int32_t* __restrict__ slot_group,
                                                             int32_t* __restrict__ slot_row,
-                                                            const int32_t* __restrict__ offsets,
+                                                            int32_t* __restrict__ counts,
+                                                            int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ perm_token, void* ws, int T,
                                                             int k, int G, int ntiles, int rows_cap) {
     const int tid = threadIdx.x;
-    if (blockIdx.x == 0) {
-        // leave the look-back state all zero for the next call
-        DispatchWs* hdr = (DispatchWs*)ws;
-        uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
-        const int n = ntiles * G;
-        for (int i = tid; i < n; i += 256) status[i] = 0ull;
-        if (tid == 0) hdr->ticket = 0;
-    }
     const int64_t o = (int64_t)blockIdx.x * 256 + tid;
+    if (permute_prologue(ws, slot_row, counts, offsets, T, k, G, ntiles, o, 1)) return;
     if (o >= (int64_t)T * k) return;
     const int g = slot_group[o];
     int row = -1;
@@ -265,6 +320,13 @@ size_t dispatch_ws_bytes(int T, int G) {
     return sizeof(DispatchWs) + ntiles * (size_t)G * sizeof(uint64_t);
 }
 
+static hipError_t clear_ws(void* ws, size_t bytes, hipStream_t s) {
+    const int64_t words = (int64_t)(bytes / 8);
+    const int64_t blocks = std::min<int64_t>((words + 255) / 256, 256);
+    hipLaunchKernelGGL(ws_clear_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (uint64_t*)ws, words);
+    return hipGetLastError();
+}
+
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
     if (a.T == 0) return hipSuccess;
     const int ntiles = ceil_div(a.T, kTile);
@@ -275,21 +337,26 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
     if (a.x_perm == nullptr) {
         const int64_t slots = (int64_t)a.T * a.k;
         hipLaunchKernelGGL(permute_index_kernel, dim3((unsigned)((slots + 255) / 256)), dim3(256), 0, s,
-                           a.slot_group, a.slot_row, a.offsets, a.perm_token, a.ws, a.T, a.k, a.G, ntiles,
-                           a.T * a.k);
-        return hipGetLastError();
+                           a.slot_group, a.slot_row, a.counts, a.offsets, a.perm_token, a.ws, a.T, a.k, a.G,
+                           ntiles, a.T * a.k);
+    } else {
+        const int nch = a.d * a.elem_bytes / 16;
+        // a row of up to 8 KB in one batch of loads per lane
+        if (nch > 256)
+            hipLaunchKernelGGL(permute_kernel<8>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                               a.slot_row, a.counts, a.offsets, a.perm_token, (const uint4*)a.x,
+                               (uint4*)a.x_perm, a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
+        else
+            hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                               a.slot_row, a.counts, a.offsets, a.perm_token, (const uint4*)a.x,
+                               (uint4*)a.x_perm, a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
     }
-    const int nch = a.d * a.elem_bytes / 16;
-    // a row of up to 8 KB in one batch of loads per lane
-    if (nch > 256)
-        hipLaunchKernelGGL(permute_kernel<8>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
-                           a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
-                           a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
-    else
-        hipLaunchKernelGGL(permute_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
-                           a.slot_row, a.offsets, a.perm_token, (const uint4*)a.x, (uint4*)a.x_perm,
-                           a.ws, a.T, a.k, a.G, nch, ntiles, a.T * a.k);
-    return hipGetLastError();
+    e = hipGetLastError();
+    // the histogram kernel ran but its partner did not: leave the workspace
+    // zero for the next call (if this launch fails too, the next call's
+    // histogram sees the stale ticket and reports it)
+    if (e != hipSuccess) (void)clear_ws(a.ws, dispatch_ws_bytes(a.T, a.G), s);
+    return e;
 }
 
 }  // namespace bmoe

@@ -24,6 +24,12 @@ def declared_functions():
     return sorted(set(re.findall(r"BMOE_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)))
 
 
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    m = re.search(r"#define BMOE_DISTILL_WS_BYTES (\d+)", text)
+    assert m and int(m.group(1)) == B.DISTILL_WS_BYTES
+
+
 def good_desc(**kw):
     d = B.make_desc(T=64, d=256, E=8, top_k=2, G=4, d_ff=512, dtype="bf16")
     return d.replace(**kw) if kw else d

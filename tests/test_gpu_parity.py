@@ -144,6 +144,38 @@ def test_dispatch_exact(name, seed):
     assert int(ws.count_nonzero()) == 0, "dispatch must leave its workspace all zero"
 
 
+def test_dispatch_reports_a_dirty_workspace():
+    """A workspace left with a stale tile ticket (as a call cut short between
+    its two kernels would leave it): the call writes the "no rows" result
+    with offsets[G] = -1 instead of stale or partial rows, leaves the
+    workspace zero, and the next call is correct. Every kernel exits
+    normally (the stale tickets are past the tile count)."""
+    L, ref = case("fine-s", 0)
+    cfg = L.cfg
+    desc = desc_of(cfg)
+    sg = torch.from_numpy(ref["slot_group"]).cuda()
+    x = dev_tensor(L.x, cfg.dtype)
+    ws = B.new_dispatch_workspace(desc, "cuda")
+    ntiles = -(-cfg.T // 256)
+    ws.view(torch.int32)[0] = ntiles + 5  # stale ticket
+    got = B.dispatch(desc, sg, x, ws)
+    torch.cuda.synchronize()
+    assert got["offsets"].cpu().numpy().tolist() == [0] * cfg.G + [-1]
+    assert int(got["counts"].abs().sum()) == 0
+    assert bool((got["slot_row"] == -1).all())
+    assert int(ws.count_nonzero()) == 0
+    got = B.dispatch(desc, sg, x, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(got["offsets"].cpu().numpy(), ref["offsets"])
+    assert np.array_equal(got["slot_row"].cpu().numpy(), ref["slot_row"])
+    for copy_rows in (False, True):  # the index-only kernel reports it the same way
+        ws.view(torch.int32)[0] = ntiles
+        got = B.dispatch(desc, sg, x if copy_rows else None, ws, copy_rows=copy_rows)
+        torch.cuda.synchronize()
+        assert int(got["offsets"][-1]) == -1 and bool((got["slot_row"] == -1).all())
+        assert int(ws.count_nonzero()) == 0
+
+
 def test_dispatch_many_tiles_and_reuse():
     """Several calls in a row on one workspace, T spanning many 256-token tiles.
 
