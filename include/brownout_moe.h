@@ -201,6 +201,27 @@ BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t*
                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * brownout_moe_dispatch_noalloc -- brownout_moe_dispatch for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same kernels and results, but
+ * the workspace is a device array inside the library, one per GPU, of
+ * BMOE_DISPATCH_SCRATCH_BYTES bytes, held until the process ends. The call
+ * allocates nothing; each call first clears the array with a kernel (no
+ * memset, so it may be captured into a graph). Arguments as for
+ * brownout_moe_dispatch without the workspace. Shapes whose workspace
+ * (bmoe_workspace_bytes(desc, BMOE_STAGE_DISPATCH)) exceeds the array return
+ * BMOE_ERR_WORKSPACE before anything is enqueued. Every call on one GPU uses
+ * that GPU's array, which keeps the last call's contents: two calls on one GPU
+ * that overlap in time (other streams, other threads) race and must not be
+ * made. The device is the current HIP device.
+ */
+#define BMOE_DISPATCH_SCRATCH_BYTES 1048576
+BMOE_API bmoe_status brownout_moe_dispatch_noalloc(const bmoe_desc* desc, const int32_t* slot_group,
+                                          const void* x, int32_t* counts, int32_t* offsets,
+                                          int32_t* perm_token, int32_t* slot_row, void* x_perm,
+                                          void* stream);
+
+/*
  * brownout_moe_ffn -- grouped SwiGLU FFN (Sec. 2.1 "small FFNs"; SwiGLU form).
  * Segment s covers rows offsets[s] .. offsets[s+1]-1 of a and uses united
  * expert s:

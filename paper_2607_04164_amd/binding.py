@@ -29,9 +29,10 @@ EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_
             "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
             "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
             "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather", "brownout_moe_united_init",
-            "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map")
+            "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map", "brownout_moe_dispatch_noalloc")
 STATUS_CODES = {v: k for k, v in STATUS.items()}
 DISTILL_WS_BYTES = 32768
+DISPATCH_SCRATCH_BYTES = 1048576  # the array behind brownout_moe_dispatch_noalloc
 
 
 class BmoeError(RuntimeError):
@@ -88,6 +89,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_route.restype = I32
     lib.brownout_moe_dispatch.argtypes = [DP] + [P] * 8 + [SZ, P]
     lib.brownout_moe_dispatch.restype = I32
+    lib.brownout_moe_dispatch_noalloc.argtypes = [DP] + [P] * 8
+    lib.brownout_moe_dispatch_noalloc.restype = I32
     lib.brownout_moe_ffn.argtypes = [I32] * 5 + [P] * 8 + [SZ, P]
     lib.brownout_moe_ffn.restype = I32
     lib.brownout_moe_ffn_ex.argtypes = [I32] * 5 + [P] * 8 + [SZ, I32, P]
@@ -214,6 +217,31 @@ def dispatch(desc: Desc, slot_group: torch.Tensor, x: Optional[torch.Tensor], wo
         _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]) if copy_rows else None, _p(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "brownout_moe_dispatch")
+    return o
+
+
+def dispatch_noalloc(desc: Desc, slot_group: torch.Tensor, x: Optional[torch.Tensor], *,
+                     out: Optional[Dict[str, torch.Tensor]] = None, copy_rows: bool = True,
+                     stream=None) -> Dict[str, torch.Tensor]:
+    """dispatch on the library's own per-device workspace array (the call
+    allocates nothing on the device; pass every output in ``out`` to keep this
+    wrapper from allocating them)."""
+    T, k, G, d = desc.T, desc.top_k, desc.G, desc.d
+    dev = slot_group.device
+    _dev(slot_group, "slot_group", torch.int32, (T, k))
+    if copy_rows or x is not None:
+        _dev(x, "x", desc.torch_dtype, (T, d))
+    o = dict(out) if out else {}
+    o.setdefault("counts", _empty((G,), torch.int32, dev))
+    o.setdefault("offsets", _empty((G + 1,), torch.int32, dev))
+    o.setdefault("perm_token", _empty((max(T * k, 1),), torch.int32, dev))
+    o.setdefault("slot_row", _empty((T, k), torch.int32, dev))
+    if copy_rows:
+        o.setdefault("x_perm", _empty((max(T * k, 1), d), desc.torch_dtype, dev))
+    st = load_library().brownout_moe_dispatch_noalloc(
+        ctypes.byref(desc), _p(slot_group), _p(x), _p(o["counts"]), _p(o["offsets"]),
+        _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]) if copy_rows else None, _stream(stream))
+    _check(st, "brownout_moe_dispatch_noalloc")
     return o
 
 

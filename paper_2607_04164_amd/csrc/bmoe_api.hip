@@ -97,6 +97,21 @@ bmoe_status brownout_moe_dispatch(const bmoe_desc* d, const int32_t* slot_group,
     return hip_status(launch_dispatch(a, (hipStream_t)stream));
 }
 
+bmoe_status brownout_moe_dispatch_noalloc(const bmoe_desc* d, const int32_t* slot_group, const void* x,
+                                          int32_t* counts, int32_t* offsets, int32_t* perm_token,
+                                          int32_t* slot_row, void* x_perm, void* stream) {
+    bmoe_status st = bmoe_validate(d);
+    if (st != BMOE_OK) return st;
+    if (d->T == 0) return BMOE_OK;
+    if (!slot_group || !counts || !offsets || !perm_token || !slot_row || (x_perm && !x))
+        return BMOE_ERR_NULL;
+    if (x_perm && (!aligned16(x) || !aligned16(x_perm))) return BMOE_ERR_ALIGN;
+    if (dispatch_ws_bytes(d->T, d->G) > (size_t)BMOE_DISPATCH_SCRATCH_BYTES) return BMOE_ERR_WORKSPACE;
+    DispatchArgs a{slot_group, x, counts, offsets, perm_token, slot_row, x_perm, nullptr,
+                   d->T, d->d, d->top_k, d->G, elem_bytes(d->dtype)};
+    return hip_status(launch_dispatch_noalloc(a, (hipStream_t)stream));
+}
+
 }  // extern "C"
 
 namespace {

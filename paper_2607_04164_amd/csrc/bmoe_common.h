@@ -181,6 +181,8 @@ struct DispatchArgs {
 };
 size_t dispatch_ws_bytes(int T, int G);
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);
+// a.ws ignored: the library's own per-device array (BMOE_DISPATCH_SCRATCH_BYTES)
+hipError_t launch_dispatch_noalloc(const DispatchArgs& a, hipStream_t s);
 
 struct FfnArgs {
     const int32_t* offsets;

@@ -17,6 +17,7 @@
 // row, writes perm_token, and copies x[t] into each of its rows with 128-bit
 // loads and stores. Workgroup 0 clears the look-back state for the next call.
 #include <algorithm>
+#include <mutex>
 
 #include "bmoe_common.h"
 #include "stream_io.h"
@@ -25,6 +26,7 @@ namespace bmoe {
 namespace {
 
 constexpr int kTile = 256;
+constexpr int kMaxDevices = 64;
 constexpr uint32_t kFlagAgg = 1u, kFlagPrefix = 2u;
 // Upper bound on polls of one predecessor's status word. Predecessors publish
 // without waiting, so the bound is only reached if the workspace was not
@@ -357,6 +359,46 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
     // histogram sees the stale ticket and reports it)
     if (e != hipSuccess) (void)clear_ws(a.ws, dispatch_ws_bytes(a.T, a.G), s);
     return e;
+}
+
+// ---- the allocation-free variant: the workspace is a device array of the
+// library itself (one copy per GPU, found through hipGetSymbolAddress once
+// per device and kept; never passed by its host-side name)
+
+static __device__ __align__(256) uint64_t scratch[BMOE_DISPATCH_SCRATCH_BYTES / 8];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+static hipError_t scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_dispatch_noalloc(const DispatchArgs& a0, hipStream_t s) {
+    if (a0.T == 0) return hipSuccess;
+    const size_t bytes = dispatch_ws_bytes(a0.T, a0.G);
+    if (bytes > (size_t)BMOE_DISPATCH_SCRATCH_BYTES) return hipErrorInvalidValue;  // checked by the caller
+    DispatchArgs a = a0;
+    hipError_t e = scratch_address(&a.ws);
+    if (e != hipSuccess) return e;
+    // every call starts from a cleared array (by a kernel, not a memset, so
+    // the call may be captured into a graph)
+    e = clear_ws(a.ws, bytes, s);
+    if (e != hipSuccess) return e;
+    return launch_dispatch(a, s);
 }
 
 }  // namespace bmoe

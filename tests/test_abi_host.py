@@ -26,6 +26,8 @@ def declared_functions():
 
 def test_header_constants_match_binding():
     text = open(HEADER).read()
+    m = re.search(r"#define BMOE_DISPATCH_SCRATCH_BYTES (\d+)", text)
+    assert m and int(m.group(1)) == B.DISPATCH_SCRATCH_BYTES
     m = re.search(r"#define BMOE_DISTILL_WS_BYTES (\d+)", text)
     assert m and int(m.group(1)) == B.DISTILL_WS_BYTES
 
@@ -116,6 +118,13 @@ def test_entry_points_reject_before_launch(lib):
     assert lib.brownout_moe_dispatch(bd, FAKE, z, FAKE, FAKE, FAKE, FAKE, z, z, need, z) == WS
     assert lib.brownout_moe_dispatch(bd, FAKE, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need, z) == NULL
     assert lib.brownout_moe_dispatch(bd, FAKE, z, z, FAKE, FAKE, FAKE, z, FAKE, need, z) == NULL
+    # allocation-free dispatch: the same checks, and shapes beyond its array
+    nd = lib.brownout_moe_dispatch_noalloc
+    assert nd(bd, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == NULL
+    assert nd(bd, FAKE, MISALIGNED, FAKE, FAKE, FAKE, FAKE, FAKE, z) == ALIGN
+    huge = good_desc(T=140000, E=256, G=256)
+    assert B.workspace_bytes(huge, B.STAGE_DISPATCH) > B.DISPATCH_SCRATCH_BYTES
+    assert nd(ctypes.byref(huge), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z) == WS
     # ffn (and its halves)
     ffn = lib.brownout_moe_ffn
     assert ffn(9, 4, 128, 256, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, z, 0, z) == UNSUP
@@ -174,6 +183,7 @@ def test_zero_tokens_needs_no_pointers(lib):
     z = None
     assert lib.brownout_moe_route(bd, z, z, z, z, z, z, z, z, z, z, z) == OK
     assert lib.brownout_moe_dispatch(bd, z, z, z, z, z, z, z, z, 0, z) == OK
+    assert lib.brownout_moe_dispatch_noalloc(bd, z, z, z, z, z, z, z, z) == OK
     assert lib.brownout_moe_combine(bd, z, z, z, z, z, z) == OK
     assert lib.brownout_moe_ffn(1, 4, 0, 256, 512, z, z, z, z, z, z, z, z, 0, z) == OK
     assert lib.brownout_moe_ffn_gather(1, 4, 0, 256, 512, z, z, 0, z, z, z, z, z, z, z, 0, z) == OK
