@@ -103,9 +103,12 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--compare-ungrouped", action="store_true",
-                    help="also time the same layer with no grouping (G = E, every expert its own group: "
-                         "zero brownout) and report the speedup of grouping")
+    ap.add_argument("--no-compare-ungrouped", action="store_true",
+                    help="skip timing the same layer with no grouping (G = E, every expert its own group: "
+                         "zero brownout) and the speedup of grouping")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the fine, heavy and decode workloads that the default (Mixtral-shaped) run "
+                         "also times")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the layer: time a device-to-device copy of this many MiB (the plain "
                          "copy kernel that HBM byte counters are calibrated against)")
@@ -135,21 +138,44 @@ def copy_probe(mib: int, reps: int = 10):
 _LAYERS = {}  # the last generated layer, reused when the same workload is timed again
 
 
-def time_layer(cfg, args, dev):
+def device_ffn_weights(cfg, seed, dev):
+    """United-expert (and shared) FFN weights drawn on the device from the
+    workload's distribution, N(0, 1/sqrt(d)) rounded to bf16: for timing-only
+    runs (the extra workloads and the ungrouped comparison), where drawing
+    gigabytes with numpy on the host would dominate the bench's run time."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(1_000_003 * seed + cfg.E * 131 + cfg.G)
+    std = 1.0 / np.sqrt(cfg.d)
+
+    def draw(shape):
+        return (torch.randn(shape, generator=g, device=dev, dtype=torch.float32) * std).to(torch.bfloat16)
+
+    G, f, d = cfg.G, cfg.d_ff, cfg.d
+    w = {"w_gate": draw((G, f, d)), "w_up": draw((G, f, d)), "w_down": draw((G, d, f))}
+    if cfg.n_shared:
+        fs = cfg.d_ff_shared
+        w.update(w_gate_sh=draw((1, fs, d)), w_up_sh=draw((1, fs, d)), w_down_sh=draw((1, d, fs)))
+    return w
+
+
+def time_layer(cfg, args, dev, device_weights=False):
     """Builds the seeded layer on the device and times args.steps full forwards
     after args.warmup untimed ones. Returns the host layer, the partial-brownout
     segment summary (or None), wall ms per step, the dominant kernel's event
-    ms, per-stage event ms in the steps, alone and (HBM stages) with cold
-    caches, the row count N, the group row counts and the stages."""
+    ms, per-stage event ms in the steps, alone and with cold caches, the row
+    count N, the group row counts and the stages. device_weights: the FFN
+    weights are drawn on the device (timing only; the route inputs still come
+    from the seeded host generator)."""
     import torch
     from paper_2607_04164_amd import binding as B
     from paper_2607_04164_amd import workload as W
 
-    key = (cfg, args.seed)
+    key = (cfg, args.seed, device_weights)
     if key not in _LAYERS:
         print(f"[bench] generating {cfg.name} (G={cfg.G}) seed {args.seed}", file=sys.stderr, flush=True)
         _LAYERS.clear()
-        _LAYERS[key] = W.make_layer(cfg, args.seed)
+        _LAYERS[key] = W.make_layer(cfg, args.seed, with_weights=not device_weights)
     L0 = L = _LAYERS[key]
     seg_info = None
     if cfg.theta is not None:
@@ -172,10 +198,15 @@ def time_layer(cfg, args, dev):
         return torch.from_numpy(a).to(dev)
 
     w = {"w_router": to_dev(L.w_router), "bias": torch.from_numpy(L.bias).to(dev),
-         "e2g": torch.from_numpy(L.e2g).to(dev), "w_gate": to_dev(L.w_gate), "w_up": to_dev(L.w_up),
-         "w_down": to_dev(L.w_down)}
-    if cfg.n_shared:
-        w.update(w_gate_sh=to_dev(L.w_gate_sh), w_up_sh=to_dev(L.w_up_sh), w_down_sh=to_dev(L.w_down_sh))
+         "e2g": torch.from_numpy(L.e2g).to(dev)}
+    if device_weights:
+        if cfg.theta is not None or cfg.dtype != "bf16":
+            raise SystemExit("device-drawn weights are for the bf16 full-brownout workloads")
+        w.update(device_ffn_weights(cfg, args.seed, dev))
+    else:
+        w.update(w_gate=to_dev(L.w_gate), w_up=to_dev(L.w_up), w_down=to_dev(L.w_down))
+        if cfg.n_shared:
+            w.update(w_gate_sh=to_dev(L.w_gate_sh), w_up_sh=to_dev(L.w_up_sh), w_down_sh=to_dev(L.w_down_sh))
     x = to_dev(L.x)
     desc = B.make_desc(cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.G, cfg.d_ff, cfg.d_ff_shared, cfg.norm_topk,
                        cfg.dtype)
@@ -278,17 +309,16 @@ def time_layer(cfg, args, dev):
             e1.record()
             torch.cuda.synchronize()
             ep_ms.append(e0.elapsed_time(e1) / 3)
-    # the HBM-bound stages once more with cold caches: before each launch a
-    # read pass over 1 GiB evicts L2 and the 256 MB MALL (a read, so no dirty
-    # lines are left to be written back inside the timed launch)
+    # every stage once more with cold caches: before each launch a read pass
+    # over 1 GiB evicts L2 and the 256 MB MALL (a read, so no dirty lines are
+    # left to be written back inside the timed launch)
     cold_ms = {}
     # float32, so that sum() is one reduction over the buffer (an integer sum
     # would first widen the whole buffer to int64, a 2 GiB write)
     flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
     for s in stages:
-        if s.startswith("ffn") or s == "shared_ffn":
-            continue
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+        reps = 3 if s.startswith("ffn") or s == "shared_ffn" else 10
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
         for e0, e1 in evs:
             flush.sum()
             e0.record()
@@ -300,6 +330,34 @@ def time_layer(cfg, args, dev):
     del layer, w, x
     torch.cuda.empty_cache()
     return L0, (cfg, seg_info, ep_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
+
+
+def ungrouped_line(cfg, args, dev, ms_grouped):
+    """The same layer with no grouping (G = E): tokens/s and the speedup of
+    the grouped layer over it."""
+    ucfg = cfg.with_(name=cfg.name + "-ungrouped", G=cfg.E, theta=None)
+    uargs = argparse.Namespace(**{**vars(args), "share": None, "fused_gather": False})
+    _, _, ms_u, _, _, iso_u, _, N_u, _, _ = time_layer(ucfg, uargs, dev, device_weights=True)
+    return {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1), "ms_per_step": round(ms_u, 4),
+            "stages_us": {k: round(v * 1e3, 2) for k, v in iso_u.items()},
+            "grouped_speedup": round(ms_u / ms_grouped, 3),
+            "note": "FFN weights drawn on the device (timing only)"}
+
+
+def dominant_rate(cfg, N, counts, dom_ms, cold_ms):
+    """The gate/up GEMM against its roofline: MFMA (4*N*d*d_ff flop, event
+    time in the steps) or, for decode-sized batches on the weight-streaming
+    kernel, HBM (weight bytes of the segments with rows, cold launch)."""
+    T, d, k, f, s = cfg.T, cfg.d, cfg.top_k, cfg.d_ff, cfg.elem_bytes
+    if T * k <= 64 * len(counts):
+        S_w = sum(1 for c in counts if c > 0)
+        by = 2 * S_w * d * f * s + N * d * s + N * f * s
+        gbs = by / (cold_ms * 1e-3) / 1e9
+        return {"kernel": "skinny_dma_kernel<gated>", "bound": "hbm", "us_cold": round(cold_ms * 1e3, 2),
+                "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    tf = 4.0 * N * d * f / (dom_ms * 1e-3) / 1e12
+    return {"kernel": "grouped_gemm_dma_kernel<gated>", "bound": "mfma", "us": round(dom_ms * 1e3, 2),
+            "TFLOP_s": round(tf, 1), "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
 
 
 def parse_share(text):
@@ -386,6 +444,10 @@ def main():
             rate = amount / (ms * 1e-3) / 1e12
             stage_out[st_name] = {"us": round(ms * 1e3, 2), "in_step_us": round(per_stage_ms[st_name] * 1e3, 2),
                                   "flop": amount, "TFLOP_s": round(rate, 1), "frac_of_peak": round(rate / peak, 4)}
+            if st_name in cold_ms:
+                cold = amount / (cold_ms[st_name] * 1e-3) / 1e12
+                stage_out[st_name].update({"cold_us": round(cold_ms[st_name] * 1e3, 2),
+                                           "cold_TFLOP_s": round(cold, 1), "cold_frac_of_peak": round(cold / peak, 4)})
 
     dom = "ffn_gate_up"
     dkind, damount = work[dom]
@@ -395,11 +457,17 @@ def main():
                if share is None and args.theta is None and not args.fused_gather else None)
     if skinny:
         dach = damount / (dms * 1e-3) / 1e9
-        roofline = {"kernel": "skinny_gemm_kernel<gated> (brownout_moe_ffn_gate_up)", "bound": "hbm",
-                    "achieved": round(dach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(dach / HBM_PEAK_GBS, 4), "traffic": traffic,
+        cach = damount / (cold_ms[dom] * 1e-3) / 1e9
+        kname = "skinny_dma_kernel" if d % 64 == 0 else "skinny_gemm_kernel"
+        # the decode weights fit the 256 MB MALL: back-to-back steps read them
+        # from there, so the HBM fraction is the cold launch's
+        roofline = {"kernel": f"{kname}<gated> (brownout_moe_ffn_gate_up)", "bound": "hbm",
+                    "achieved": round(cach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(cach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "warm_achieved": round(dach, 1), "warm_frac": round(dach / HBM_PEAK_GBS, 4),
                     "per_launch": f"weights 2*S*d*d_ff*s with S={S_w} segments with rows, plus N*d*s rows read and "
-                                  f"N*d_ff*s written, N={N}"}
+                                  f"N*d_ff*s written, N={N}; achieved from cold launches (after a 1 GiB read "
+                                  f"pass), warm_* from the timed steps (weights served from the MALL)"}
     else:
         dpeak = MFMA_BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
         dach = damount / (dms * 1e-3) / 1e12
@@ -428,6 +496,9 @@ def main():
                    "rows_N": N, "group_rows": counts},
         "roofline": roofline,
         "stages": stage_out,
+        "stages_note": "us / rates: the stage launched alone back to back (warm: activations, and weights "
+                       "below 256 MB, may be served from the 256 MB MALL); in_step_us: inside the timed steps; "
+                       "cold_*: median launch after a 1 GiB read pass that evicts L2 and the MALL",
         "cpu_baseline": None,
     }
 
@@ -465,15 +536,31 @@ def main():
                                   "note": "dispatch writes only the permutation; the gate/up GEMM gathers "
                                           "its rows from x"}
 
-    if args.compare_ungrouped and cfg0.G != cfg0.E:
+    plain = share is None and args.theta is None and not args.fused_gather and cfg0.dtype == "bf16"
+    if plain and not args.no_compare_ungrouped and cfg0.G != cfg0.E:
         # zero brownout on the same layer: every expert its own group
-        ucfg = cfg0.with_(name=cfg0.name + "-ungrouped", G=cfg0.E, theta=None)
-        uargs = argparse.Namespace(**{**vars(args), "share": None})
-        _, _, ms_u, _, stages_u, _, _, N_u, _, _ = time_layer(ucfg, uargs, dev)
-        result["ungrouped"] = {"G": cfg.E, "rows_N": N_u, "value": round(cfg.T / (ms_u * 1e-3), 1),
-                               "ms_per_step": round(ms_u, 4),
-                               "stages_us": {k: round(v * 1e3, 2) for k, v in stages_u.items()},
-                               "grouped_speedup": round(ms_u / ms_step, 3)}
+        result["ungrouped"] = ungrouped_line(cfg0, args, dev, ms_step)
+
+    if plain and args.config == "mixtral" and not args.no_extra:
+        # the other full-size workloads, grouped and ungrouped, in the same run
+        result["other_workloads"] = {}
+        for name in ("fine", "heavy", "decode"):
+            wcfg = W.CONFIGS[name]
+            xargs = argparse.Namespace(**{**vars(args), "share": None, "fused_gather": False})
+            _, _, ms_w, dom_w, _, iso_w, cold_w, N_w, counts_w, _ = time_layer(wcfg, xargs, dev,
+                                                                                 device_weights=True)
+            line = {"workload": WORKLOAD_TEXT[name], "value": round(wcfg.T / (ms_w * 1e-3), 1),
+                    "unit": "tokens/s", "ms_per_step": round(ms_w, 4), "rows_N": N_w,
+                    "dominant": dominant_rate(wcfg, N_w, counts_w, dom_w, cold_w["ffn_gate_up"]),
+                    "stages_us": {k: round(v * 1e3, 2) for k, v in iso_w.items()},
+                    "stages_cold_us": {k: round(v * 1e3, 2) for k, v in cold_w.items()}}
+            line["ungrouped"] = ungrouped_line(wcfg, xargs, dev, ms_w)
+            result["other_workloads"][name] = line
+        result["other_workloads_note"] = ("same kernels and bench protocol; united-expert weights drawn on the "
+                                          "device from the workload's distribution (route inputs from the seeded "
+                                          "host generator); ungrouped: G = E, every expert its own group (zero "
+                                          "brownout), the in-framework analogue of the paper's grouped-vs-unfused "
+                                          "comparison (Sec. 5), not comparable with its numbers")
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(L, cfg0, share, args.share_rank, args.cpu_seconds)
@@ -579,9 +666,63 @@ def bench_distill(args, dev):
     print(json.dumps(result), flush=True)
 
 
+def host_cpu():
+    """The host's CPU model, logical CPUs and the CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
+
+
+def oracle_layer_timed(Lf):
+    """The oracle's whole layer (the same stage calls as oracle.layer), each
+    stage timed; returns (seconds per stage, total seconds)."""
+    import oracle
+    cfg = Lf.cfg
+    st = {}
+    t = time.perf_counter()
+    x = Lf.x
+    r = oracle.route(x, Lf.w_router, Lf.bias, Lf.e2g, cfg.top_k, cfg.norm_topk)
+    st["route"] = time.perf_counter() - t
+    t = time.perf_counter()
+    dsp = oracle.dispatch(r["slot_group"], cfg.G)
+    xp = oracle.gather_rows(x, dsp["perm_token"])
+    st["dispatch"] = time.perf_counter() - t
+    t = time.perf_counter()
+    y = oracle.ffn(dsp["offsets"], xp, Lf.w_gate, Lf.w_up, Lf.w_down)
+    st["ffn"] = time.perf_counter() - t
+    y_sh = None
+    if cfg.n_shared:
+        t = time.perf_counter()
+        y_sh = oracle.ffn(np.array([0, cfg.T], np.int32), x, Lf.w_gate_sh, Lf.w_up_sh, Lf.w_down_sh)
+        st["shared_ffn"] = time.perf_counter() - t
+    t = time.perf_counter()
+    oracle.combine(dsp["slot_row"], r["slot_gate"], y, y_sh, d=cfg.d)
+    st["combine"] = time.perf_counter() - t
+    return st, sum(st.values())
+
+
+def widen(L):
+    """The layer with its bf16 storage widened to the float32 the oracle reads."""
+    import dataclasses
+    names = ("x", "w_router", "w_gate", "w_up", "w_down", "w_gate_sh", "w_up_sh", "w_down_sh")
+    return dataclasses.replace(L, cfg=L.cfg.with_(dtype="f32"), **{k: L.f32(k) for k in names})
+
+
 def cpu_baseline(L, cfg, share, rank, budget_s):
     """The CPU oracle, unchanged, on a bounded sample of the same tokens (of
-    the same share of the layer when it is sharded)."""
+    the same share of the layer when it is sharded), stage by stage; and, for
+    reference, the whole tiny and decode workloads on one thread and on all."""
     import dataclasses
 
     import oracle
@@ -598,24 +739,41 @@ def cpu_baseline(L, cfg, share, rank, budget_s):
         cfg = L.cfg
 
     # widen the bf16 storage to the float32 the oracle reads, once, outside the timing
-    names = ("x", "w_router", "w_gate", "w_up", "w_down", "w_gate_sh", "w_up_sh", "w_down_sh")
-    Lf = dataclasses.replace(L, cfg=cfg.with_(dtype="f32"), **{k: L.f32(k) for k in names})
+    Lf = widen(L)
 
     def run(n):
         sub = dataclasses.replace(Lf, cfg=Lf.cfg.with_(T=n), x=Lf.x[:n])
-        t = time.perf_counter()
-        oracle.layer(sub)
-        return time.perf_counter() - t
+        return oracle_layer_timed(sub)
 
     print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-    run(min(4, cfg.T))  # widen weights / warm caches once
+    run(min(4, cfg.T))  # warm caches once
     n0 = min(16, cfg.T)
-    t0 = run(n0)
+    st, t0 = run(n0)
     n = int(min(cfg.T, max(n0, n0 * budget_s / max(t0, 1e-6))))
-    t = run(n) if n != n0 else t0
-    return {"value": round(n / t, 2), "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"first {n} of {cfg.T} tokens of the same workload, whole layer "
-                      f"(route, dispatch, FFN, combine), {t:.1f} s wall"}
+    if n != n0:
+        st, t = run(n)
+    else:
+        t = t0
+    threads = oracle.num_threads()
+    out = {"value": round(n / t, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"first {n} of {cfg.T} tokens of the same workload, whole layer "
+                     f"(route, dispatch, FFN, combine), {t:.1f} s wall on {threads} threads",
+           "stages_s": {k: round(v, 4) for k, v in st.items()}}
+    out.update(host_cpu())
+    # whole small workloads, one thread and all threads
+    single = {}
+    for name in ("tiny", "decode"):
+        Ls = widen(W.make_layer(W.CONFIGS[name], 0))
+        row = {}
+        for nt in (1, threads):
+            oracle.set_num_threads(nt)
+            oracle_layer_timed(Ls)  # warm
+            best = min(oracle_layer_timed(Ls)[1] for _ in range(3))
+            row[f"tokens_s_{nt}_threads"] = round(Ls.cfg.T / best, 2)
+        oracle.set_num_threads(threads)
+        single[name] = row
+    out["whole_small_workloads"] = single
+    return out
 
 
 if __name__ == "__main__":

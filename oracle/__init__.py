@@ -61,6 +61,7 @@ class Oracle:
         P = ctypes.c_void_p
         I = ctypes.c_int
         lib.oracle_num_threads.restype = I
+        lib.oracle_set_num_threads.argtypes = [I]
         lib.oracle_router_logits.argtypes = [P, P, P, I, I, I, P]
         lib.oracle_route_from_logits.argtypes = [P, P, I, I, I, I, P, P, P, P]
         lib.oracle_route_from_logits_f32.argtypes = [P, P, I, I, I, I, P, P, P, P]
@@ -74,6 +75,9 @@ class Oracle:
 
     def num_threads(self) -> int:
         return int(self.lib.oracle_num_threads())
+
+    def set_num_threads(self, n: int) -> None:
+        self.lib.oracle_set_num_threads(int(n))
 
     def router_logits(self, x, w_router, bias=None) -> np.ndarray:
         x, w, b = _f32(x), _f32(w_router), _f32(bias)
@@ -202,6 +206,7 @@ def _fwd(name):
 
 
 num_threads = _fwd("num_threads")
+set_num_threads = _fwd("set_num_threads")
 router_logits = _fwd("router_logits")
 route_from_logits = _fwd("route_from_logits")
 route = _fwd("route")

@@ -56,6 +56,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads the following calls may use (timing runs only; no effect on results). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Gate logits (Sec. 2.1 "gating function"; linear router reading).
  * z[t*E+e] = sum_j x[t*d+j] * w[e*d+j]  (+ bias[e]), double, ascending j.   */

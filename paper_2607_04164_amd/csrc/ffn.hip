@@ -410,13 +410,28 @@ __device__ __forceinline__ void dma_stage(const DmaSrc<C>& src, uint32_t stage_l
     for (int i = 0; i < C::DMA_PER_STAGE; ++i) dma_one<C>(src, stage_lds, wave, kb, i);
 }
 
+// First tile row of 32-row block mb of wave row wm. The blocks of the two
+// wave rows interleave (block 2*mb + wm), so the valid rows of a segment's
+// last, partly filled tile are shared by both wave rows, and each skips the
+// MFMAs of its blocks that lie wholly past the segment (see dma_valid_blocks).
+template <class C>
+__device__ __forceinline__ int dma_arow(int wm, int mb) { return (2 * mb + wm) * 32; }
+
+// Blocks of wave row wm that hold at least one row of the tile's segment
+// (a wave-uniform count in 0..MB).
+template <class C>
+__device__ __forceinline__ int dma_valid_blocks(int m0, int m_end, int wm) {
+    const int nvb = min(max(m_end - m0, 0) + 31, 2 * C::MB * 32) / 32;  // blocks with a valid row
+    return (nvb - wm + 1) / 2;
+}
+
 template <class C>
 __device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB], const char* stage,
                                           int wm, int wn, int lane, int kk) {
     const int c = kk * 2 + (lane >> 5), l32 = lane & 31;
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb)
-        af[mb] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + mb * 32 + l32, c));
+        af[mb] = *(const uint4*)(stage + lds_off<C>(dma_arow<C>(wm, mb) + l32, c));
 #pragma unroll
     for (int mat = 0; mat < C::NMAT; ++mat)
 #pragma unroll
@@ -433,7 +448,7 @@ __device__ __forceinline__ void frag_read(uint4 (&ga)[C::MB], uint4 (&gb)[C::NMA
         gb[rm][rn] = *(const uint4*)(stage + C::A_STAGE + lds_off<C>(rm * C::BN + wn * C::WTN + rn * 32 + l32, c));
     } else {
         const int ra = r - C::NMAT * C::NB;
-        ga[ra] = *(const uint4*)(stage + lds_off<C>(wm * C::WTM + ra * 32 + l32, c));
+        ga[ra] = *(const uint4*)(stage + lds_off<C>(dma_arow<C>(wm, ra) + l32, c));
     }
 }
 
@@ -443,7 +458,7 @@ __device__ __forceinline__ void frag_read(uint4 (&ga)[C::MB], uint4 (&gb)[C::NMA
 // (DMA instructions d0 .. d0 + ND - 1), one after every (NM / ND)-th MFMA.
 // (Issuing a sub-step's copies after each of its first MFMAs instead
 // measured 1-3 % slower: the copies must be spread.)
-template <class C, int RD, int ND>
+template <class C, int RD, int ND, int MBV>
 __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
                                           const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga1)[C::MB],
                                           uint4 (&gb1)[C::NMAT][C::NB], const char* st1, int kk1,
@@ -458,7 +473,8 @@ __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
         const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
-        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        // blocks wholly past the segment's last row: no MFMA
+        if (mb < MBV) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (RD == 2) {
             if (q < NR) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q);
@@ -588,7 +604,7 @@ enum { kAfterNone = 0, kAfterStores = 1 };
 // K-steps [ka, kb) of one tile into acc (which the caller zeroed), after
 // ksteps_prologue. Ends with every copy complete and a barrier, so the LDS
 // ring may be reused.
-template <class C>
+template <class C, int MBV>
 __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
                                             char* smem, int ka, int kb, int wave, int lane, int after) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
@@ -624,23 +640,23 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
         const int kb = (ka + kt + 2) * C::BK * 2;
         constexpr int D1 = 6, D2 = 5, D3 = C::DMA_PER_STAGE - D1 - D2;
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, 0>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
+        mfmas_ops<C, 2, 0, MBV>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
                            dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
         lds_reads_done();
         wg_barrier();  // the slot is free
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 0, DMA ? D1 : 0>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
+        mfmas_ops<C, 0, DMA ? D1 : 0, MBV>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
                                       src, dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 0, DMA ? D2 : 0>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
+        mfmas_ops<C, 0, DMA ? D2 : 0, MBV>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
                                       src, dma_lds, wave, kb, D1);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (DMA) wait_vmcnt<D1 + D2>();
         else wait_vmcnt<0>();
         wg_barrier();  // the next K-step is resident
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, DMA ? D3 : 0>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
+        mfmas_ops<C, 2, DMA ? D3 : 0, MBV>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
                                       src, dma_lds, wave, kb, D1 + D2);
         __builtin_amdgcn_sched_barrier(0);
     };
@@ -648,6 +664,21 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
     for (; kt < n; ++kt) kstep(kt, std::false_type{});
     __syncthreads();
+}
+
+// tile_ksteps for a wave with mbv valid 32-row blocks (the MFMAs of the
+// others are left out at compile time: a run-time test around each MFMA made
+// the compiler move the accumulators out of their registers)
+template <class C>
+__device__ __forceinline__ void tile_ksteps_mbv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
+                                                char* smem, int ka, int kb, int wave, int lane, int after,
+                                                int mbv) {
+    static_assert(C::MB == 4, "four 32-row blocks per wave");
+    if (mbv >= 4) tile_ksteps<C, 4>(acc, src, smem, ka, kb, wave, lane, after);
+    else if (mbv == 3) tile_ksteps<C, 3>(acc, src, smem, ka, kb, wave, lane, after);
+    else if (mbv == 2) tile_ksteps<C, 2>(acc, src, smem, ka, kb, wave, lane, after);
+    else if (mbv == 1) tile_ksteps<C, 1>(acc, src, smem, ka, kb, wave, lane, after);
+    else tile_ksteps<C, 0>(acc, src, smem, ka, kb, wave, lane, after);
 }
 
 template <class C>
@@ -686,7 +717,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
     const int wm = wave >> 1, wn = wave & 1;
     uint16_t* st = (uint16_t*)(smem + C::STG_OFF + wave * C::HSTG);
     const int l32 = lane & 31;
-    const int row0 = tc.m0 + wm * C::WTM, col0 = tc.n0 + wn * C::WTN;
+    const int row0 = tc.m0, col0 = tc.n0 + wn * C::WTN;
     if (piece) {
         float4* d = (float4*)piece;
 #pragma unroll
@@ -708,7 +739,8 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
         return;
     }
 #pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
+    for (int mb = 0; mb < C::MB; ++mb) {
+        if (row0 + dma_arow<C>(wm, mb) >= tc.m_end) continue;  // a block wholly past the segment
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             // rows 16h .. 16h+15 of the 32-row block: accumulator elements 8h .. 8h+7
@@ -737,11 +769,12 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
             for (int k = 0; k < 16 * C::CPR / 64; ++k) {
                 const int c = lane + 64 * k;
                 const int rr = c / C::CPR, cc = c % C::CPR;
-                const int gm = row0 + mb * 32 + 16 * h + rr, gn = col0 + cc * 8;
+                const int gm = row0 + dma_arow<C>(wm, mb) + 16 * h + rr, gn = col0 + cc * 8;
                 const uint4 v = *(const uint4*)(st + rr * C::SROW + cc * 8);
                 if (gm < tc.m_end && gn < p.N) *(uint4*)(p.C + (size_t)gm * p.N + gn) = v;
             }
         }
+    }
     __builtin_amdgcn_sched_barrier(0);
 }
 
@@ -795,7 +828,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         dma_sources<C, GATED>(src, p, tc, wave, lane);
         zero_acc<C>(acc);
         ksteps_prologue<C>(src, smem, 0, nk, wave);
-        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone);
+        tile_ksteps_mbv<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone,
+                           dma_valid_blocks<C>(tc.m0, tc.m_end, wave >> 1));
         store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
     } else {
         const int P = gridDim.x;
@@ -840,7 +874,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         int after = kAfterNone;
         while (L >= 0) {
             zero_acc<C>(acc);
-            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane, after);
+            tile_ksteps_mbv<C>(acc, src, smem, ka, kb, wave, lane, after,
+                               dma_valid_blocks<C>(tc.m0, tc.m_end, wave >> 1));
             int L2, ka2, kb2, slot2;
             next_item(L2, ka2, kb2, slot2);
             TileCoord tc2;
@@ -951,7 +986,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_fixup_kernel(GemmParams p, 
     for (int k = 0; k < QPER; ++k) {
         const int qq = qs * QPER + k;  // slot (mb, nb, i4) in the order of store_piece
         const int i4 = qq & 3, nb = (qq >> 2) % C::NB, mb = (qq >> 2) / C::NB;
-        const int r0 = wm * C::WTM + mb * 32 + 8 * i4 + 4 * (lane >> 5);
+        const int r0 = dma_arow<C>(wm, mb) + 8 * i4 + 4 * (lane >> 5);
         const int gn = tc.n0 + wn * C::WTN + nb * 32 + (lane & 31);
         const float g4[4] = {sum[k][0].x, sum[k][0].y, sum[k][0].z, sum[k][0].w};
         const float4 u = sum[k][C::NMAT - 1];
