@@ -56,9 +56,11 @@ extern "C" {
 #define BMOE_MAX_TOPK 16     /* top_k <= 16 */
 
 /* Route decides every token whose fast fp32 logits leave any two of its top
- * (k+1) values closer than this gap (2^-12) again from float64 logits; see
- * brownout_moe_route. */
-#define BMOE_ROUTE_RECHECK_GAP (1.0f / 4096.0f)
+ * (k+1) values closer than this gap (2^-14) again from float64 logits; see
+ * brownout_moe_route. The gap is far above the error of the fp32 logits (a few
+ * 1e-6 at d = 4096), so every pair the fp32 logits order is ordered the same
+ * way by the float64 ones. */
+#define BMOE_ROUTE_RECHECK_GAP (1.0f / 16384.0f)
 
 typedef enum bmoe_status {
     BMOE_OK = 0,

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libbrownout_moe.so")
 
 BMOE_F32, BMOE_BF16 = 0, 1
 STAGE_ROUTE, STAGE_DISPATCH, STAGE_FFN, STAGE_COMBINE = 0, 1, 2, 3
-ROUTE_RECHECK_GAP = 1.0 / 4096.0
+ROUTE_RECHECK_GAP = 1.0 / 16384.0
 MAX_EXPERTS, MAX_TOPK = 256, 16
 
 STATUS = {0: "BMOE_OK", 1: "BMOE_ERR_NULL", 2: "BMOE_ERR_SHAPE", 3: "BMOE_ERR_ALIGN",

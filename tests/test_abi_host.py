@@ -30,6 +30,8 @@ def test_header_constants_match_binding():
     assert m and int(m.group(1)) == B.DISPATCH_SCRATCH_BYTES
     m = re.search(r"#define BMOE_DISTILL_WS_BYTES (\d+)", text)
     assert m and int(m.group(1)) == B.DISTILL_WS_BYTES
+    m = re.search(r"#define BMOE_ROUTE_RECHECK_GAP \(1\.0f / (\d+)\.0f\)", text)
+    assert m and 1.0 / int(m.group(1)) == B.ROUTE_RECHECK_GAP
 
 
 def good_desc(**kw):

@@ -90,10 +90,12 @@ def test_route_exact(name, seed):
     assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
 
 
-def test_route_near_ties_decided_in_f64():
+@pytest.mark.parametrize("E,d", [(16, 256), (8, 256), (8, 4096)], ids=["mfma-E16", "valu-E8", "valu-E8-d4096"])
+def test_route_near_ties_decided_in_f64(E, d):
     """Two experts whose logits differ by far less than the fp32 rounding error
-    (and exact ties) are still ordered as float64 orders them."""
-    cfg = W.LayerConfig("ties", T=96, d=256, E=16, top_k=4, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
+    (and exact ties) are still ordered as float64 orders them (on the MFMA
+    logits path and on the dot-product path of routers with few experts)."""
+    cfg = W.LayerConfig("ties", T=96, d=d, E=E, top_k=4, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
     L = W.make_layer(cfg, 5)
     # expert 7's router row equals expert 3's except one bf16 ulp in column 17;
     # column 17 of x is tiny, so the two logits differ by |x[t,17]| * ulp
