@@ -97,6 +97,8 @@ def parse():
                          "calibration set, the routing-weighted distillation errors)")
     ap.add_argument("--no-compare-fused", action="store_true",
                     help="skip the second timing of the same layer on the fused-gather path")
+    ap.add_argument("--no-compare-fold", action="store_true",
+                    help="skip timing the layer with the combine folded into the down projection")
     ap.add_argument("--theta", type=float, default=None,
                     help="partial-brownout threshold in [0, 1] (overrides the workload's; "
                          "0 is full brownout, 1 zero brownout)")
@@ -211,14 +213,21 @@ def time_layer(cfg, args, dev, device_weights=False):
     desc = B.make_desc(cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.G, cfg.d_ff, cfg.d_ff_shared, cfg.norm_topk,
                        cfg.dtype)
     fused = bool(getattr(args, "fused_gather", False))
-    layer = B.LayerForward(desc, w, device=dev, fused_gather=fused)
+    fold = bool(getattr(args, "fold_combine", False))
+    layer = B.LayerForward(desc, w, device=dev, fused_gather=fused, fold_combine=fold,
+                           stream_k=not getattr(args, "no_stream_k", False))
 
-    stages = ["route", "dispatch", "ffn_gate_up", "ffn_down"] + (["shared_ffn"] if cfg.n_shared else []) + \
-             ["combine"]
+    if fold:
+        # the shared experts' output feeds the folded combine
+        stages = ["route", "dispatch", "ffn_gate_up"] + (["shared_ffn"] if cfg.n_shared else []) + ["down_combine"]
+    else:
+        stages = ["route", "dispatch", "ffn_gate_up", "ffn_down"] + (["shared_ffn"] if cfg.n_shared else []) + \
+                 ["combine"]
     calls = {"route": lambda: layer.route(x), "dispatch": lambda: layer.dispatch(x),
              "ffn_gate_up": (lambda: layer.ffn_gate_up(x=x)) if fused else layer.ffn_gate_up,
              "ffn_down": layer.ffn_down,
-             "shared_ffn": lambda: layer.shared(x), "combine": layer.combine}
+             "shared_ffn": lambda: layer.shared(x), "combine": layer.combine,
+             "down_combine": layer.down_combine if fold else None}
 
     def step(events=None):
         for i, s in enumerate(stages):
@@ -269,7 +278,7 @@ def time_layer(cfg, args, dev, device_weights=False):
     # hold the gaps between kernels, which dominate the short stages)
     iso_ms = {}
     for s in stages:
-        reps = 3 if s.startswith("ffn") or s == "shared_ffn" else 20
+        reps = 3 if s.startswith("ffn") or s in ("shared_ffn", "down_combine") else 20
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         calls[s]()
         torch.cuda.synchronize()
@@ -317,7 +326,7 @@ def time_layer(cfg, args, dev, device_weights=False):
     # would first widen the whole buffer to int64, a 2 GiB write)
     flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
     for s in stages:
-        reps = 3 if s.startswith("ffn") or s == "shared_ffn" else 10
+        reps = 3 if s.startswith("ffn") or s in ("shared_ffn", "down_combine") else 10
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
         for e0, e1 in evs:
             flush.sum()
@@ -535,6 +544,23 @@ def main():
                                   "speedup": round(ms_step / ms_f, 3),
                                   "note": "dispatch writes only the permutation; the gate/up GEMM gathers "
                                           "its rows from x"}
+
+    if not args.fused_gather and not args.no_compare_fold and share is None and cfg0.dtype == "bf16":
+        # the combine folded into the down projection (no stream-K split of its
+        # tiles), beside the same layer unfused and without the split
+        fargs = argparse.Namespace(**{**vars(args), "fold_combine": True})
+        _, _, ms_f, _, _, iso_f, cold_f, _, _, _ = time_layer(cfg0, fargs, dev)
+        nargs = argparse.Namespace(**{**vars(args), "no_stream_k": True})
+        _, _, ms_n, _, _, iso_n, _, _, _, _ = time_layer(cfg0, nargs, dev)
+        result["fold_combine"] = {"value": round(cfg.T / (ms_f * 1e-3), 1), "ms_per_step": round(ms_f, 4),
+                                  "stages_us": {k: round(v * 1e3, 2) for k, v in iso_f.items()},
+                                  "speedup": round(ms_step / ms_f, 3),
+                                  "unsplit_unfused": {"value": round(cfg.T / (ms_n * 1e-3), 1),
+                                                      "ms_per_step": round(ms_n, 4),
+                                                      "stages_us": {k: round(v * 1e3, 2) for k, v in iso_n.items()}},
+                                  "note": "down projection with the combine in its epilogue (tiles never split); "
+                                          "unsplit_unfused: the four-call layer without the stream-K workspace, "
+                                          "which the fold reproduces bit for bit"}
 
     plain = share is None and args.theta is None and not args.fused_gather and cfg0.dtype == "bf16"
     if plain and not args.no_compare_ungrouped and cfg0.G != cfg0.E:

@@ -82,7 +82,8 @@ typedef enum bmoe_stage {
     BMOE_STAGE_ROUTE = 0,
     BMOE_STAGE_DISPATCH = 1,
     BMOE_STAGE_FFN = 2,
-    BMOE_STAGE_COMBINE = 3
+    BMOE_STAGE_COMBINE = 3,
+    BMOE_STAGE_DOWN_COMBINE = 4  /* brownout_moe_ffn_down_combine */
 } bmoe_stage;
 
 /* Shape of one layer. */
@@ -346,6 +347,31 @@ BMOE_API bmoe_status brownout_moe_distill_mse(int32_t dtype, int32_t E, int32_t 
                                      const int32_t* e2g, const float* w_freq, const void* y_expert,
                                      const void* y_united, double* mse, double* mse_total, void* workspace,
                                      size_t workspace_bytes, void* stream);
+
+/*
+ * brownout_moe_ffn_down_combine -- the down projection with the combine folded
+ * into its epilogue (the fused MoE operator of Sec. 4.1; the layer output of
+ * Sec. 2.1). Writes the same y as brownout_moe_ffn_down and the same out, bit
+ * for bit, as brownout_moe_combine on that y (fp32 fmaf of slot gate and bf16
+ * y over the token's valid slots in slot order, + y_shared, one RNE rounding),
+ * whatever order the tiles finish in: each tile's epilogue counts its rows per
+ * (token, 128-column chunk), and the row that completes a token's chunk forms
+ * that chunk of out from the token's rows of y.
+ * desc: the layer (G segments, d, d_ff, top_k, dtype). offsets [G+1], h
+ * [T*k, d_ff], w_down [G, d, d_ff], y [T*k, d], perm_token [T*k], slot_row
+ * [T,k], slot_gate [T,k] (as written by route and dispatch), y_shared [T,d] or
+ * NULL, out [T,d]. workspace: bmoe_workspace_bytes(desc,
+ * BMOE_STAGE_DOWN_COMBINE) bytes (4 * T * ceil(d/128)), 256-byte aligned, ALL
+ * ZERO before the first call; every call leaves it zero; calls that share one
+ * must not overlap. The fold runs on the 256-row bf16 GEMM tiles with d a
+ * multiple of 128 (every tile whole: no stream-K split); other shapes run the
+ * down projection and then the combine kernel, with the same results.
+ */
+BMOE_API bmoe_status brownout_moe_ffn_down_combine(const bmoe_desc* desc, const int32_t* offsets, const void* h,
+                                          const void* w_down, void* y, const int32_t* perm_token,
+                                          const int32_t* slot_row, const float* slot_gate,
+                                          const void* y_shared, void* out, void* workspace,
+                                          size_t workspace_bytes, void* stream);
 
 /*
  * brownout_moe_combine -- weighted sum back into token order (Sec. 2.1: the

@@ -18,7 +18,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libbrownout_moe.so")
 
 BMOE_F32, BMOE_BF16 = 0, 1
-STAGE_ROUTE, STAGE_DISPATCH, STAGE_FFN, STAGE_COMBINE = 0, 1, 2, 3
+STAGE_ROUTE, STAGE_DISPATCH, STAGE_FFN, STAGE_COMBINE, STAGE_DOWN_COMBINE = 0, 1, 2, 3, 4
 ROUTE_RECHECK_GAP = 1.0 / 16384.0
 MAX_EXPERTS, MAX_TOPK = 256, 16
 
@@ -29,7 +29,7 @@ EXPORTED = ("bmoe_validate", "bmoe_validate_map", "bmoe_workspace_bytes", "bmoe_
             "bmoe_version", "brownout_moe_route", "brownout_moe_dispatch", "brownout_moe_ffn",
             "brownout_moe_ffn_gate_up", "brownout_moe_ffn_down", "brownout_moe_combine",
             "brownout_moe_ffn_gather", "brownout_moe_ffn_gate_up_gather", "brownout_moe_united_init",
-            "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map", "brownout_moe_dispatch_noalloc")
+            "brownout_moe_distill_mse", "brownout_moe_ffn_ex", "bmoe_partial_segment_map", "brownout_moe_dispatch_noalloc", "brownout_moe_ffn_down_combine")
 STATUS_CODES = {v: k for k, v in STATUS.items()}
 DISTILL_WS_BYTES = 32768
 DISPATCH_SCRATCH_BYTES = 1048576  # the array behind brownout_moe_dispatch_noalloc
@@ -109,6 +109,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.brownout_moe_ffn_down.restype = I32
     lib.brownout_moe_combine.argtypes = [DP] + [P] * 6
     lib.brownout_moe_combine.restype = I32
+    lib.brownout_moe_ffn_down_combine.argtypes = [DP] + [P] * 10 + [SZ, P]
+    lib.brownout_moe_ffn_down_combine.restype = I32
     lib.bmoe_partial_segment_map.argtypes = [P, P, I32, I32, ctypes.c_double, P, P, P, P]
     lib.bmoe_partial_segment_map.restype = I32
     _lib = lib
@@ -241,7 +243,7 @@ def dispatch_noalloc(desc: Desc, slot_group: torch.Tensor, x: Optional[torch.Ten
     st = load_library().brownout_moe_dispatch_noalloc(
         ctypes.byref(desc), _p(slot_group), _p(x), _p(o["counts"]), _p(o["offsets"]),
         _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]) if copy_rows else None, _stream(stream))
-    _check(st, "brownout_moe_dispatch_noalloc")
+    _check(st, "brownout_moe_dispatch_noalloc", "brownout_moe_ffn_down_combine")
     return o
 
 
@@ -454,6 +456,38 @@ def combine(desc: Desc, slot_row: torch.Tensor, slot_gate: torch.Tensor, y_perm:
     return out
 
 
+def new_down_combine_workspace(desc: Desc, device) -> torch.Tensor:
+    """The all-zero counter workspace of ffn_down_combine (kept zero by every call)."""
+    n = workspace_bytes(desc, STAGE_DOWN_COMBINE)
+    return torch.zeros((n + 255) // 256 * 256, dtype=torch.uint8, device=device)
+
+
+def ffn_down_combine(desc: Desc, offsets, h, w_down, perm_token, slot_row, slot_gate, workspace,
+                     y_shared=None, *, y=None, out=None, stream=None):
+    """The down projection with the combine folded into its epilogue:
+    returns (y, out), bit-identical to ffn_down (without a stream-K workspace)
+    followed by combine."""
+    T, k, d, G, f = desc.T, desc.top_k, desc.d, desc.G, desc.d_ff
+    dt = desc.torch_dtype
+    rows = max(T * k, 1)
+    _dev(offsets, "offsets", torch.int32, (G + 1,))
+    _dev(h, "h", dt, (rows, f))
+    _dev(w_down, "w_down", dt, (G, d, f))
+    _dev(perm_token, "perm_token", torch.int32, (rows,))
+    _dev(slot_row, "slot_row", torch.int32, (T, k))
+    _dev(slot_gate, "slot_gate", torch.float32, (T, k))
+    _dev(workspace, "workspace", torch.uint8)
+    if y_shared is not None:
+        _dev(y_shared, "y_shared", dt, (T, d))
+    y = _dev(y, "y", dt, (rows, d)) if y is not None else _empty((rows, d), dt, h.device)
+    out = _dev(out, "out", dt, (T, d)) if out is not None else _empty((T, d), dt, h.device)
+    st = load_library().brownout_moe_ffn_down_combine(
+        ctypes.byref(desc), _p(offsets), _p(h), _p(w_down), _p(y), _p(perm_token), _p(slot_row), _p(slot_gate),
+        _p(y_shared), _p(out), _p(workspace), workspace.numel(), _stream(stream))
+    _check(st, "brownout_moe_ffn_down_combine")
+    return y, out
+
+
 # ---------------------------------------------------------------------------
 
 class LayerForward:
@@ -472,13 +506,18 @@ class LayerForward:
     fused_gather=True: dispatch writes only the permutation and the gate/up
     GEMM gathers its rows from x (no x_perm buffer); ffn and ffn_gate_up then
     take x. Results are bit-identical to the unfused path.
+
+    fold_combine=True: the combine runs in the down projection's epilogue
+    (brownout_moe_ffn_down_combine; its tiles are never split, so the layer
+    equals the unfused layer without the stream-K workspace, bit for bit).
     """
 
     def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True,
-                 fused_gather: bool = False):
+                 fused_gather: bool = False, fold_combine: bool = False):
         self.desc = desc
         self.w = weights
         self.fused_gather = fused_gather
+        self.fold_combine = fold_combine
         _check(validate(desc), "bmoe_validate")
         T, k, d, G, E = desc.T, desc.top_k, desc.d, desc.G, desc.E
         dt = desc.torch_dtype
@@ -499,6 +538,7 @@ class LayerForward:
             self.bufs["dispatch"]["x_perm"] = _empty((rows, d), dt, device)
         self.ws = new_dispatch_workspace(desc, device)
         self.ffn_ws = new_ffn_workspace(desc, device) if stream_k else None
+        self.fold_ws = new_down_combine_workspace(desc, device) if fold_combine else None
         if desc.d_ff_shared:
             self.bufs["h_sh"] = _empty((max(T, 1), desc.d_ff_shared), dt, device)
             self.bufs["y_sh"] = _empty((max(T, 1), d), dt, device)
@@ -541,6 +581,11 @@ class LayerForward:
         self._a_at = 8 if fused else None  # where x's pointer goes in the fused argument lists
         self._combine_args = (ptr(dp["slot_row"]), ptr(r["slot_gate"]), ptr(b["y"]),
                               ptr(b["y_sh"]) if desc.d_ff_shared else None, ptr(b["out"]))
+        if self.fold_combine:
+            self._down_combine_args = (ptr(dp["offsets"]), ptr(b["h"]), ptr(w["w_down"]), ptr(b["y"]),
+                                       ptr(dp["perm_token"]), ptr(dp["slot_row"]), ptr(r["slot_gate"]),
+                                       ptr(b["y_sh"]) if desc.d_ff_shared else None, ptr(b["out"]),
+                                       ptr(self.fold_ws), self.fold_ws.numel())
         if desc.d_ff_shared:
             fs = desc.d_ff_shared
             _dev(w["w_gate_sh"], "w_gate_sh", dt, (1, fs, d))
@@ -608,9 +653,20 @@ class LayerForward:
                "brownout_moe_combine")
         return self.bufs["out"]
 
+    def down_combine(self, stream=None):
+        """The down projection with the combine folded in (fold_combine layers)."""
+        _check(self._lib.brownout_moe_ffn_down_combine(self._desc_ref, *self._down_combine_args, self._s(stream)),
+               "brownout_moe_ffn_down_combine")
+        return self.bufs["out"]
+
     def __call__(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         self.route(x, stream)
         self.dispatch(x, stream)
+        if self.fold_combine:
+            self.ffn_gate_up(stream, x=x)
+            if self.desc.d_ff_shared:
+                self.shared(x, stream)
+            return self.down_combine(stream)
         self.ffn(stream, x=x)
         if self.desc.d_ff_shared:
             self.shared(x, stream)

@@ -61,6 +61,7 @@ size_t bmoe_workspace_bytes(const bmoe_desc* d, int32_t stage) {
     if (bmoe_validate(d) != BMOE_OK) return 0;
     if (stage == BMOE_STAGE_DISPATCH) return dispatch_ws_bytes(d->T, d->G);
     if (stage == BMOE_STAGE_FFN && d->dtype == BMOE_BF16) return ffn_workspace_bytes();
+    if (stage == BMOE_STAGE_DOWN_COMBINE) return down_combine_ws_bytes(d->T, d->d);
     return 0;
 }
 
@@ -202,6 +203,40 @@ bmoe_status brownout_moe_ffn_down(int32_t dtype, int32_t n_seg, int32_t rows_cap
     // h is only read by the down GEMM
     return ffn_common(2, dtype, n_seg, rows_cap, d, d_ff, offsets, nullptr, nullptr, nullptr, w_down,
                       const_cast<void*>(h), y, workspace, workspace_bytes, stream);
+}
+
+bmoe_status brownout_moe_ffn_down_combine(const bmoe_desc* d, const int32_t* offsets, const void* h,
+                                          const void* w_down, void* y, const int32_t* perm_token,
+                                          const int32_t* slot_row, const float* slot_gate, const void* y_shared,
+                                          void* out, void* workspace, size_t workspace_bytes, void* stream) {
+    bmoe_status st = bmoe_validate(d);
+    if (st != BMOE_OK) return st;
+    if (d->T == 0) return BMOE_OK;
+    if (!offsets || !h || !w_down || !y || !perm_token || !slot_row || !slot_gate || !out) return BMOE_ERR_NULL;
+    if (!aligned16(h) || !aligned16(w_down) || !aligned16(y) || !aligned16(out) ||
+        (y_shared && !aligned16(y_shared)))
+        return BMOE_ERR_ALIGN;
+    const int32_t rows_cap = d->T * d->top_k;
+    if ((int64_t)rows_cap * (d->d > d->d_ff ? d->d : d->d_ff) > ((int64_t)1 << 40)) return BMOE_ERR_SHAPE;
+    if (!workspace || workspace_bytes < down_combine_ws_bytes(d->T, d->d)) return BMOE_ERR_WORKSPACE;
+    if ((uintptr_t)workspace & 255u) return BMOE_ERR_ALIGN;
+    FfnArgs args{offsets, nullptr, nullptr, nullptr, w_down, const_cast<void*>(h), y, nullptr, 0,
+                 d->G, rows_cap, d->d, d->d_ff, d->dtype};
+    args.fold.perm_token = perm_token;
+    args.fold.slot_row = slot_row;
+    args.fold.slot_gate = slot_gate;
+    args.fold.y_shared = (const uint16_t*)y_shared;
+    args.fold.out = (uint16_t*)out;
+    args.fold.cnt = (int32_t*)workspace;
+    args.fold.k = d->top_k;
+    if (ffn_can_fold(args)) return hip_status(launch_ffn(args, (hipStream_t)stream, 2));
+    // other shapes: the down projection, then the combine kernel
+    args.fold = FoldArgs{};
+    hipError_t e = launch_ffn(args, (hipStream_t)stream, 2);
+    if (e != hipSuccess) return BMOE_ERR_HIP;
+    CombineArgs c{slot_row, slot_gate, y, y_shared, out, d->T, d->top_k, d->d, elem_bytes(d->dtype),
+                  (int64_t)rows_cap};
+    return hip_status(launch_combine(c, (hipStream_t)stream));
 }
 
 bmoe_status brownout_moe_united_init(int32_t dtype, int32_t E, int32_t G, int32_t d, int32_t d_ff,

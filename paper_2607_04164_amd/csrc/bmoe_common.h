@@ -184,6 +184,17 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);
 // a.ws ignored: the library's own per-device array (BMOE_DISPATCH_SCRATCH_BYTES)
 hipError_t launch_dispatch_noalloc(const DispatchArgs& a, hipStream_t s);
 
+// Combine folded into the down projection (out == nullptr: not folded).
+struct FoldArgs {
+    const int32_t* perm_token = nullptr;  // [rows]: token of each row
+    const int32_t* slot_row = nullptr;    // [T, k]
+    const float* slot_gate = nullptr;     // [T, k]
+    const uint16_t* y_shared = nullptr;   // [T, d] bf16 or nullptr
+    uint16_t* out = nullptr;              // [T, d] bf16
+    int32_t* cnt = nullptr;               // [T, d / 128] counters, zero between calls
+    int k = 0;
+};
+
 struct FfnArgs {
     const int32_t* offsets;
     const void* a;
@@ -202,7 +213,13 @@ struct FfnArgs {
     // stream-K split threshold in K-steps of average idle time per workgroup
     // (negative: the library default)
     int split_min_idle = -1;
+    FoldArgs fold;
 };
+// whether launch_ffn folds the combine into the down projection for these
+// arguments (bf16 256-row tiles, d a multiple of 128)
+bool ffn_can_fold(const FfnArgs& a);
+// counters of the folded combine: one int per (token, 128-column chunk)
+inline size_t down_combine_ws_bytes(int T, int d) { return (size_t)4 * (T > 0 ? T : 1) * ((d + 127) / 128); }
 
 // Row of the A operand that GEMM row r reads: a_rows[r] clamped into the
 // source, or r itself when the operand is not gathered.

@@ -39,6 +39,7 @@ struct GemmParams {
     int sk_min_idle;  // stream-K split threshold (average idle K-steps per workgroup)
     const int32_t* a_rows = nullptr;  // gathered A: row r is A[a_rows[r]] (A has a_count rows)
     int a_count = 0;
+    FoldArgs fold;  // combine folded into the down projection's epilogue (out == nullptr: not folded)
 };
 
 template <bool GATED, int BM, int BN, int BK>
@@ -710,7 +711,101 @@ __device__ __forceinline__ float acc_read(float a) {
 // (lane-interleaved float4, the layout the fixup reads). One routine for
 // both, block by block: with two routines the compiler moved every
 // accumulator out of the AGPRs where the paths split and spilled.
-template <class C, bool GATED>
+// ---- combine folded into the down projection's epilogue
+//
+// y is still written (as the unfused path writes it), with stores that are
+// coherent across the XCDs' L2 caches (sc1: written through to the device's
+// coherence point). Once a wave's stores of its 128 columns are complete, it
+// counts each of its rows in a counter per (token, 128-column chunk); the row
+// that brings a counter to the token's number of rows completes that chunk of
+// the token, and its wave forms the chunk of out exactly as the combine kernel
+// would: fp32 fmaf of slot gate and bf16 y over the token's valid slots in
+// slot order (+ the shared-expert output), one RNE rounding. The other rows
+// of the token are read with coherent (sc1) loads; the counter is left zero.
+// Whatever order the rows arrive in, out is bit-identical to the unfused
+// combine.
+typedef uint32_t fold_u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void store_coherent(uint16_t* p, const uint4& v) {
+    const fold_u32x4 w = __builtin_bit_cast(fold_u32x4, v);
+    asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(w) : "memory");
+}
+__device__ __forceinline__ uint4 load_coherent(const uint16_t* p) {
+    fold_u32x4 w;
+    asm volatile("global_load_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "=v"(w) : "v"(p) : "memory");
+    return __builtin_bit_cast(uint4, w);
+}
+
+// The wave's 128 rows of one tile, columns [c0, c0 + 128) of y, are written
+// (and complete): count them, and finish the token chunks they complete.
+template <class C>
+__device__ __forceinline__ void fold_rows(const GemmParams& p, const TileCoord& tc, int wm, int c0, int lane) {
+    const FoldArgs& f = p.fold;
+    if (c0 >= p.N) return;  // the wave's columns lie past the row end
+    const int k = f.k, chunk = c0 / 128, nchunk = p.N / 128;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+        const int lr = hh * 64 + lane;  // the wave's local row
+        const int gm = tc.m0 + dma_arow<C>(wm, lr / 32) + lr % 32;
+        bool last = false;
+        int t = 0;
+        if (gm < tc.m_end) {
+            t = f.perm_token[gm];
+            int nrow = 0;
+            for (int i = 0; i < k; ++i) nrow += f.slot_row[(size_t)t * k + i] >= 0 ? 1 : 0;
+            const int old = __hip_atomic_fetch_add(f.cnt + (size_t)t * nchunk + chunk, 1, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+            last = old == nrow - 1;
+        }
+        // the completed chunks, four at a time (16 lanes of 8 columns each)
+        uint64_t m = __ballot(last);
+        while (m != 0ull) {
+            // lane group grp takes the grp-th lowest completing row (if any)
+            const int grp = lane >> 4, j = lane & 15;
+            uint64_t mm = m;
+            for (int q = 0; q < grp; ++q) mm &= mm - 1ull;
+            const int src = mm != 0ull ? __ffsll((unsigned long long)mm) - 1 : -1;
+            for (int q = 0; q < 4; ++q) m &= m - 1ull;  // (m &= m - 1 is a no-op once m is 0)
+            const int tt = __shfl(t, src < 0 ? 0 : src);
+            if (src < 0) continue;
+            const int col = c0 + j * 8;
+            float acc[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+            for (int i = 0; i < k; ++i) {
+                const int r = f.slot_row[(size_t)tt * k + i];
+                if (r < 0) continue;
+                const float g = f.slot_gate[(size_t)tt * k + i];
+                const uint4 v = load_coherent(p.C + (size_t)r * p.N + col);
+                const uint32_t* u = (const uint32_t*)&v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[2 * e] = fmaf(g, __uint_as_float(u[e] << 16), acc[2 * e]);
+                    acc[2 * e + 1] = fmaf(g, __uint_as_float(u[e] & 0xffff0000u), acc[2 * e + 1]);
+                }
+            }
+            if (f.y_shared) {
+                const uint4 v = *(const uint4*)(f.y_shared + (size_t)tt * p.N + col);
+                const uint32_t* u = (const uint32_t*)&v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[2 * e] += __uint_as_float(u[e] << 16);
+                    acc[2 * e + 1] += __uint_as_float(u[e] & 0xffff0000u);
+                }
+            }
+            uint4 o;
+            o.x = pack_bf16x2(acc[0], acc[1]);
+            o.y = pack_bf16x2(acc[2], acc[3]);
+            o.z = pack_bf16x2(acc[4], acc[5]);
+            o.w = pack_bf16x2(acc[6], acc[7]);
+            *(uint4*)(f.out + (size_t)tt * p.N + col) = o;
+            if (j == 0)
+                __hip_atomic_store(f.cnt + (size_t)tt * nchunk + chunk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+template <class C, bool GATED, bool FOLD = false>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C::NB], const GemmParams& p,
                                            const TileCoord& tc, char* smem, int wave, int lane,
                                            char* piece = nullptr) {
@@ -771,11 +866,19 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
                 const int rr = c / C::CPR, cc = c % C::CPR;
                 const int gm = row0 + dma_arow<C>(wm, mb) + 16 * h + rr, gn = col0 + cc * 8;
                 const uint4 v = *(const uint4*)(st + rr * C::SROW + cc * 8);
-                if (gm < tc.m_end && gn < p.N) *(uint4*)(p.C + (size_t)gm * p.N + gn) = v;
+                if (gm < tc.m_end && gn < p.N) {
+                    if constexpr (FOLD) store_coherent(p.C + (size_t)gm * p.N + gn, v);
+                    else *(uint4*)(p.C + (size_t)gm * p.N + gn) = v;
+                }
             }
         }
     }
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (FOLD) {
+        static_assert(!GATED && C::WTN == 128, "the fold works on the down projection's 128-column wave tiles");
+        wait_vmcnt<0>();  // this wave's y stores are complete at the coherence point
+        fold_rows<C>(p, tc, wm, col0, lane);
+    }
 }
 
 // Work of P persistent workgroups: F rounds of one tile each (round r, tile
@@ -811,7 +914,7 @@ __device__ __forceinline__ SkSplit sk_split(int total, int nk, int P, bool can_s
     return k;
 }
 
-template <bool GATED, bool SK>
+template <bool GATED, bool SK, bool FOLD = false>
 __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmParams p, char* ws) {
     using C = DmaCfg<GATED>;
     __shared__ __align__(16) char smem[C::SMEM];
@@ -830,7 +933,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         ksteps_prologue<C>(src, smem, 0, nk, wave);
         tile_ksteps_mbv<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone,
                            dma_valid_blocks<C>(tc.m0, tc.m_end, wave >> 1));
-        store_tile<C, GATED>(acc, p, tc, smem, wave, lane);
+        store_tile<C, GATED, FOLD>(acc, p, tc, smem, wave, lane);
     } else {
         const int P = gridDim.x;
         const int pw = xcd_swizzle(blockIdx.x, P);
@@ -884,8 +987,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
                 dma_sources<C, GATED>(src, p, tc2, wave, lane);
                 ksteps_prologue<C>(src, smem, ka2, kb2, wave);
             }
-            store_tile<C, GATED>(acc, p, tc, smem, wave, lane,
-                                 slot < 0 ? nullptr : ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
+            store_tile<C, GATED, FOLD>(acc, p, tc, smem, wave, lane,
+                                       slot < 0 ? nullptr : ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
             after = kAfterStores;
             L = L2;
             ka = ka2;
@@ -1020,6 +1123,15 @@ hipError_t launch_gemm_dma(const GemmParams& g0, void* ws, size_t ws_bytes, hipS
     g.sk_min_idle = g0.sk_min_idle < 0 ? kSkMinIdle : g0.sk_min_idle;
     // persistent: one workgroup per CU, each XCD a contiguous range of tiles
     const int P = stream_k_workgroups();
+    if constexpr (!GATED) {
+        if (g.fold.out != nullptr) {
+            // the fold needs every tile whole (no stream-K pieces)
+            if (P <= 0) return hipErrorInvalidValue;
+            hipLaunchKernelGGL((grouped_gemm_dma_kernel<false, true, true>), dim3(P), dim3(kGemmThreads), 0, s, g,
+                               (char*)nullptr);
+            return hipGetLastError();
+        }
+    }
     if (P > 0) {
         const bool split = ws != nullptr && ws_bytes >= (size_t)2 * P * kSkSlotBytes;
         hipLaunchKernelGGL((grouped_gemm_dma_kernel<GATED, true>), dim3(P), dim3(kGemmThreads), 0, s, g,
@@ -1107,6 +1219,11 @@ static int ffn_tile(const FfnArgs& a) {
     return (a.d % kDmaBK == 0 && a.d_ff % kDmaBK == 0) ? kTileDma : kTile256;
 }
 
+bool ffn_can_fold(const FfnArgs& a) {
+    return a.dtype == BMOE_BF16 && a.rows_cap > 0 && !ffn_skinny_fits(a) && ffn_tile(a) == kTileDma &&
+           a.d % 128 == 0 && stream_k_workgroups() > 0;
+}
+
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
     if (a.rows_cap == 0) return hipSuccess;
     const bool up = part != 2, down = part != 1;
@@ -1144,6 +1261,7 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s, int part) {
         GemmParams g2{(const uint16_t*)a.h, (const uint16_t*)a.w_down, nullptr, (uint16_t*)a.y,
                       a.offsets, a.n_seg, a.rows_cap, a.d, a.d_ff};
         g2.sk_min_idle = a.split_min_idle;
+        g2.fold = a.fold;
         return tile == kTileDma   ? launch_gemm_dma<false>(g2, a.ws, a.ws_bytes, s)
                : tile == kTile256 ? launch_gemm<false, 256, 256, 64, kFdb256>(g2, s)
                                   : launch_gemm<false, 128, 256, 64, true>(g2, s);

@@ -602,6 +602,47 @@ def test_full_size_fused_gather_bit_identical(name):
 
 
 # ---------------------------------------------------------------------------
+# combine folded into the down projection's epilogue
+
+FOLD = {
+    # 256-row tiles with d a multiple of 128: the fold runs in the GEMM epilogue
+    "dma": W.LayerConfig("dma", T=2100, d=256, E=8, top_k=2, G=4, d_ff=384, dtype="bf16", zipf_s=0.5),
+    "dma-k1": W.LayerConfig("dma-k1", T=4500, d=384, E=8, top_k=1, G=4, d_ff=256, dtype="bf16", zipf_s=0.5),
+    "dma-shared": W.LayerConfig("dma-shared", T=1200, d=256, E=16, top_k=6, G=4, d_ff=256, dtype="bf16",
+                                zipf_s=1.5, n_shared=2, d_ff_shared_each=128),
+    # other shapes: the down projection, then the combine kernel
+    "mixtral-s": SMALL["mixtral-s"],
+    "tiny": SMALL["tiny"],
+}
+
+
+@pytest.mark.parametrize("name", list(FOLD))
+def test_layer_fold_combine(name):
+    """The layer with the combine folded into the down projection: the same
+    y and out bits as the unfused layer without the stream-K workspace (the
+    fold never splits a tile), within tolerance of the oracle, on two calls
+    in a row (the counter workspace is left zero)."""
+    cfg = FOLD[name]
+    L = W.make_layer(cfg, 4)
+    ref = oracle.layer(L, want_intermediates=True)
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    base = B.LayerForward(desc_of(cfg), w, stream_k=False)
+    out0 = base(x).clone()
+    y0 = base.bufs["y"].clone()
+    fold = B.LayerForward(desc_of(cfg), w, fold_combine=True)
+    for _ in range(2):
+        fold.bufs["out"].fill_(7.0)
+        out1 = fold(x)
+        torch.cuda.synchronize()
+        N = ref["N"]
+        assert torch.equal(fold.bufs["y"][:N], y0[:N])
+        assert torch.equal(out1, out0)
+        assert int(fold.fold_ws.count_nonzero()) == 0, "the counters must be left zero"
+    check_layer(L, ref, fold, out1)
+
+
+# ---------------------------------------------------------------------------
 # one GPU's share of a layer sharded over several GPUs
 
 @pytest.mark.parametrize("base,P,r", [("mixtral-s", 8, 0), ("mixtral-s", 8, 7), ("heavy-s", 4, 2)])
@@ -744,6 +785,22 @@ def test_full_size_sampled(name):
     if name == "mixtral":
         # the down GEMM's last partial round is split at this shape
         assert n_split > 0
+
+
+def test_full_size_fold_combine_bit_identical():
+    """The Mixtral-shaped layer with the combine folded into the down
+    projection writes the same out bits as the unfused layer without the
+    stream-K workspace (whose parity with the oracle the sampled tests check)."""
+    L = full_case("mixtral")
+    cfg = L.cfg
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    out0 = B.LayerForward(desc_of(cfg), w, stream_k=False)(x).clone()
+    fold = B.LayerForward(desc_of(cfg), w, fold_combine=True)
+    out1 = fold(x)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out0)
+    assert int(fold.fold_ws.count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("seed", [1, 2])
