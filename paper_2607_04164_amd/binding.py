@@ -243,7 +243,7 @@ def dispatch_noalloc(desc: Desc, slot_group: torch.Tensor, x: Optional[torch.Ten
     st = load_library().brownout_moe_dispatch_noalloc(
         ctypes.byref(desc), _p(slot_group), _p(x), _p(o["counts"]), _p(o["offsets"]),
         _p(o["perm_token"]), _p(o["slot_row"]), _p(o["x_perm"]) if copy_rows else None, _stream(stream))
-    _check(st, "brownout_moe_dispatch_noalloc", "brownout_moe_ffn_down_combine")
+    _check(st, "brownout_moe_dispatch_noalloc")
     return o
 
 
