@@ -411,20 +411,13 @@ __device__ __forceinline__ void dma_stage(const DmaSrc<C>& src, uint32_t stage_l
     for (int i = 0; i < C::DMA_PER_STAGE; ++i) dma_one<C>(src, stage_lds, wave, kb, i);
 }
 
-// First tile row of 32-row block mb of wave row wm. The blocks of the two
-// wave rows interleave (block 2*mb + wm), so the valid rows of a segment's
-// last, partly filled tile are shared by both wave rows, and each skips the
-// MFMAs of its blocks that lie wholly past the segment (see dma_valid_blocks).
+// First tile row of 32-row block mb of wave row wm. (Interleaving the two
+// wave rows' blocks and leaving out the MFMAs of blocks wholly past a
+// segment's end made the partly filled last tiles of the segments run ahead
+// of the others: the workgroups of an XCD then drifted apart along K, and the
+// gate/up GEMM's L2 misses doubled. Every tile keeps the full MFMA work.)
 template <class C>
-__device__ __forceinline__ int dma_arow(int wm, int mb) { return (2 * mb + wm) * 32; }
-
-// Blocks of wave row wm that hold at least one row of the tile's segment
-// (a wave-uniform count in 0..MB).
-template <class C>
-__device__ __forceinline__ int dma_valid_blocks(int m0, int m_end, int wm) {
-    const int nvb = min(max(m_end - m0, 0) + 31, 2 * C::MB * 32) / 32;  // blocks with a valid row
-    return (nvb - wm + 1) / 2;
-}
+__device__ __forceinline__ int dma_arow(int wm, int mb) { return wm * C::WTM + mb * 32; }
 
 template <class C>
 __device__ __forceinline__ void dma_frags(uint4 (&af)[C::MB], uint4 (&bf)[C::NMAT][C::NB], const char* stage,
@@ -459,7 +452,7 @@ __device__ __forceinline__ void frag_read(uint4 (&ga)[C::MB], uint4 (&gb)[C::NMA
 // (DMA instructions d0 .. d0 + ND - 1), one after every (NM / ND)-th MFMA.
 // (Issuing a sub-step's copies after each of its first MFMAs instead
 // measured 1-3 % slower: the copies must be spread.)
-template <class C, int RD, int ND, int MBV>
+template <class C, int RD, int ND>
 __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const uint4 (&af)[C::MB],
                                           const uint4 (&bf)[C::NMAT][C::NB], uint4 (&ga1)[C::MB],
                                           uint4 (&gb1)[C::NMAT][C::NB], const char* st1, int kk1,
@@ -474,8 +467,7 @@ __device__ __forceinline__ void mfmas_ops(f32x16 (&acc)[C::NMAT][C::MB][C::NB], 
 #pragma unroll
     for (int q = 0; q < NM; ++q) {
         const int mb = q / (C::NMAT * C::NB), mat = (q / C::NB) % C::NMAT, nb = q % C::NB;
-        // blocks wholly past the segment's last row: no MFMA
-        if (mb < MBV) acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
+        acc[mat][mb][nb] = mfma32(af[mb], bf[mat][nb], acc[mat][mb][nb]);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (RD == 2) {
             if (q < NR) frag_read<C>(ga1, gb1, st1, wm, wn, l32, c1, q);
@@ -605,7 +597,7 @@ enum { kAfterNone = 0, kAfterStores = 1 };
 // K-steps [ka, kb) of one tile into acc (which the caller zeroed), after
 // ksteps_prologue. Ends with every copy complete and a barrier, so the LDS
 // ring may be reused.
-template <class C, int MBV>
+template <class C>
 __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
                                             char* smem, int ka, int kb, int wave, int lane, int after) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
@@ -641,23 +633,23 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
         const int kb = (ka + kt + 2) * C::BK * 2;
         constexpr int D1 = 6, D2 = 5, D3 = C::DMA_PER_STAGE - D1 - D2;
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, 0, MBV>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
+        mfmas_ops<C, 2, 0>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
                            dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
         lds_reads_done();
         wg_barrier();  // the slot is free
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 0, DMA ? D1 : 0, MBV>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
+        mfmas_ops<C, 0, DMA ? D1 : 0>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
                                       src, dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 0, DMA ? D2 : 0, MBV>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
+        mfmas_ops<C, 0, DMA ? D2 : 0>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
                                       src, dma_lds, wave, kb, D1);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (DMA) wait_vmcnt<D1 + D2>();
         else wait_vmcnt<0>();
         wg_barrier();  // the next K-step is resident
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, DMA ? D3 : 0, MBV>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
+        mfmas_ops<C, 2, DMA ? D3 : 0>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
                                       src, dma_lds, wave, kb, D1 + D2);
         __builtin_amdgcn_sched_barrier(0);
     };
@@ -665,21 +657,6 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
     for (; kt < n; ++kt) kstep(kt, std::false_type{});
     __syncthreads();
-}
-
-// tile_ksteps for a wave with mbv valid 32-row blocks (the MFMAs of the
-// others are left out at compile time: a run-time test around each MFMA made
-// the compiler move the accumulators out of their registers)
-template <class C>
-__device__ __forceinline__ void tile_ksteps_mbv(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
-                                                char* smem, int ka, int kb, int wave, int lane, int after,
-                                                int mbv) {
-    static_assert(C::MB == 4, "four 32-row blocks per wave");
-    if (mbv >= 4) tile_ksteps<C, 4>(acc, src, smem, ka, kb, wave, lane, after);
-    else if (mbv == 3) tile_ksteps<C, 3>(acc, src, smem, ka, kb, wave, lane, after);
-    else if (mbv == 2) tile_ksteps<C, 2>(acc, src, smem, ka, kb, wave, lane, after);
-    else if (mbv == 1) tile_ksteps<C, 1>(acc, src, smem, ka, kb, wave, lane, after);
-    else tile_ksteps<C, 0>(acc, src, smem, ka, kb, wave, lane, after);
 }
 
 template <class C>
@@ -931,8 +908,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         dma_sources<C, GATED>(src, p, tc, wave, lane);
         zero_acc<C>(acc);
         ksteps_prologue<C>(src, smem, 0, nk, wave);
-        tile_ksteps_mbv<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone,
-                           dma_valid_blocks<C>(tc.m0, tc.m_end, wave >> 1));
+        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone);
         store_tile<C, GATED, FOLD>(acc, p, tc, smem, wave, lane);
     } else {
         const int P = gridDim.x;
@@ -977,8 +953,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         int after = kAfterNone;
         while (L >= 0) {
             zero_acc<C>(acc);
-            tile_ksteps_mbv<C>(acc, src, smem, ka, kb, wave, lane, after,
-                               dma_valid_blocks<C>(tc.m0, tc.m_end, wave >> 1));
+            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane, after);
             int L2, ka2, kb2, slot2;
             next_item(L2, ka2, kb2, slot2);
             TileCoord tc2;
