@@ -9,6 +9,10 @@
 //              16x16x32 bf16 MFMA, fp32 accumulate; with KS > 1 the waves
 //              split the d axis and their partial tiles are summed in LDS
 //              in a fixed order;
+//        bf16, E <= 8, d a multiple of 1024 up to 4096: 16 tokens, the
+//              waves split d; each wave loads its x columns straight into
+//              registers (all at once) and copies its W_router columns into
+//              its own LDS area, so the copy phase has no barrier;
 //        f32:  one (token, expert) dot product per thread;
 //        logits_in: copied.
 //   2. per token, a group of S lanes (S <= 16, chosen so that a wave's tokens
@@ -37,7 +41,16 @@ constexpr float kGap = BMOE_ROUTE_RECHECK_GAP;
 constexpr int kMaxK = BMOE_MAX_TOPK;
 static_assert(BMOE_MAX_EXPERTS <= kRouteThreads, "one map entry per thread");
 
-enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2 };
+// MODE_BF16: x and W_router through the LDS ring; MODE_BF16_RES: x straight
+// into registers, each wave's columns of W_router in its own LDS area (E <= 8,
+// d = 1024 * NBAT, NBAT <= 4)
+enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2, MODE_BF16_RES = 3 };
+__host__ __device__ constexpr bool mode_bf16(int mode) { return mode == MODE_BF16 || mode == MODE_BF16_RES; }
+
+// LDS of the router columns (8 rows of d, four wave areas) and of the
+// partial logit tiles of waves 1..3
+__host__ __device__ inline size_t res_w_bytes(int d) { return (size_t)8 * d * 2; }
+constexpr size_t kResPartBytes = 3 * 16 * 16 * 4;
 
 struct RouteSmem {
     int zstride;
@@ -72,16 +85,18 @@ struct RouteCfg {
 };
 
 template <int MODE, int TB, int NBLK, int KW>
-__host__ __device__ inline RouteSmem route_smem(int E) {
+__host__ __device__ inline RouteSmem route_smem(int E, int d) {
     RouteSmem s;
     const int bt = 16 * TB;
-    const int e_pad = (MODE == MODE_BF16) ? 16 * NBLK : ((E + 15) / 16) * 16;
+    const int e_pad = mode_bf16(MODE) ? 16 * NBLK : ((E + 15) / 16) * 16;
     s.zstride = e_pad + 1;
     s.zs_bytes = ((size_t)bt * s.zstride * 4 + 15) / 16 * 16;
     s.flag_bytes = 2048;
     s.cand_bytes = 4 * 2048;
     s.dummy_bytes = (MODE == MODE_BF16) ? 4 * 1024 : 0;
-    s.ring_bytes = (MODE == MODE_BF16) ? (size_t)RouteCfg<TB, NBLK, KW>::NSLOT * RouteCfg<TB, NBLK, KW>::SLOT : 0;
+    s.ring_bytes = 0;
+    if constexpr (MODE == MODE_BF16) s.ring_bytes = (size_t)RouteCfg<TB, NBLK, KW>::NSLOT * RouteCfg<TB, NBLK, KW>::SLOT;
+    if constexpr (MODE == MODE_BF16_RES) s.ring_bytes = res_w_bytes(d) + kResPartBytes;
     return s;
 }
 
@@ -220,6 +235,57 @@ __device__ __forceinline__ void finish_token(const RouteArgs& p, int t, int s, i
     }
 }
 
+// The same from picks held in registers (k <= kRegK; every lane of the
+// token's group holds all of them): no memory round trips and no branches
+// but the stores. Sums are taken in the same order as above, so the results
+// are the same bits.
+constexpr int kRegK = 8;
+template <typename V>
+__device__ __forceinline__ void finish_regs(const RouteArgs& p, int t, int s, int S, const int (&hk)[kRegK],
+                                            const V (&hv)[kRegK], float sum_exp, bool write) {
+    const int k = p.k;
+    float ex[kRegK];
+    int g[kRegK];
+    float tot = 0.f;
+#pragma unroll
+    for (int j = 0; j < kRegK; ++j) {
+        const bool in = j < k;
+        ex[j] = in ? __expf((float)(hv[j] - hv[0])) : 0.f;
+        g[j] = in ? pick_group(hk[j]) : -2 - j;  // never equal to a pick's group
+        tot += ex[j];
+    }
+    if (!write) return;
+    const float inv = 1.f / (p.norm ? tot : sum_exp);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = s + i * S;
+        int kq = kNoPick, gq = -2 - kRegK;
+        float eq = 0.f;
+#pragma unroll
+        for (int j = 0; j < kRegK; ++j) {
+            kq = j == q ? hk[j] : kq;
+            gq = j == q ? g[j] : gq;
+            eq = j == q ? ex[j] : eq;
+        }
+        float gs = 0.f;
+        bool dup = false;
+#pragma unroll
+        for (int j = 0; j < kRegK; ++j) {
+            const bool same = g[j] == gq;
+            dup = dup || (same && j < q);
+            gs += (same && j >= q) ? ex[j] : 0.f;
+        }
+        if (q < k) {
+            const size_t o = (size_t)t * k + q;
+            p.topk_idx[o] = pick_expert(kq);
+            p.topk_w[o] = eq * inv;
+            const bool valid = !dup && gq >= 0;
+            p.slot_group[o] = valid ? gq : -1;
+            p.slot_gate[o] = valid ? gs * inv : 0.f;
+        }
+    }
+}
+
 // Step 2 for the TPW tokens of one wave. Groups of S lanes are independent
 // (their exchanges stay inside the group), so a group without a token idles.
 struct SelectCtx {
@@ -263,11 +329,20 @@ __device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCt
             const float z = c.zs[tl * c.zstride + e];
             v[j] = j < vpl ? z : -INFINITY;
         }
-        // the picks go to the pick area (every lane of the group writes the
-        // same values); registers indexed by the round would need dynamic
-        // register indexing
+        // with k <= kRegK every lane of the group keeps the picks in registers
+        // (each pick goes to its slot by a select per slot, so no register is
+        // indexed by the round); larger k use the pick area (every lane of the
+        // group writes the same values)
         int* pk = c.area + tw * 32;
         float* pkv = (float*)(pk + 16);
+        int hk[kRegK];
+        float hv[kRegK];
+#pragma unroll
+        for (int j = 0; j < kRegK; ++j) {
+            hk[j] = kNoPick;
+            hv[j] = 0.f;
+        }
+        const bool regs = k <= kRegK;
         unsigned taken = dead;
         float prev = 0.f, top = 0.f, kth = 0.f;
         bool close = false;
@@ -285,7 +360,13 @@ __device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCt
             group_argmax<S>(bv, be);
             const int e = pick_expert(be);
             if ((e & (S - 1)) == s) taken |= 1u << ((e / S) & 31);
-            if (r < k) {
+            if (regs) {
+#pragma unroll
+                for (int j = 0; j < kRegK; ++j) {
+                    hk[j] = r == j ? be : hk[j];
+                    hv[j] = r == j ? bv : hv[j];
+                }
+            } else if (r < k) {
                 pk[r] = be;
                 pkv[r] = bv;
             }
@@ -299,7 +380,8 @@ __device__ __forceinline__ void select_tokens(const RouteArgs& p, const SelectCt
 #pragma unroll
         for (int j = 0; j < V; ++j) se += j < vpl ? __expf(v[j] - top) : 0.f;
         se = group_sum<S>(se);
-        finish_token<float>(p, c.t0 + tl, s, S, pk, pkv, top, se, tok_ok && !close);
+        if (regs) finish_regs(p, c.t0 + tl, s, S, hk, hv, se, tok_ok && !close);
+        else finish_token<float>(p, c.t0 + tl, s, S, pk, pkv, top, se, tok_ok && !close);
         if (tok_ok && close && s == 0) {
             const int pos = atomicAdd(c.fl_count, 1);
             c.fl_tok[pos] = tl;
@@ -322,6 +404,7 @@ __device__ __forceinline__ void select_tokens_v(const RouteArgs& p, const Select
     } else {
         if (vpl <= 1) select_tokens<S, 1, TPW>(p, c, lane);
         else if (vpl <= 4) select_tokens<S, 4, TPW>(p, c, lane);
+        else if (vpl <= 8) select_tokens<S, 8, TPW>(p, c, lane);
         else select_tokens<S, 16, TPW>(p, c, lane);
     }
 }
@@ -337,7 +420,7 @@ template <int MODE>
 __device__ __forceinline__ void dot_f64_range(const char* xr, const char* w, size_t row_bytes, int cb, int ce,
                                               const int (&ids)[8], int lane, double (&out)[8]) {
     constexpr int U = 2;
-    constexpr int EPC = MODE == MODE_BF16 ? 8 : 4;  // elements per 16-byte chunk
+    constexpr int EPC = mode_bf16(MODE) ? 8 : 4;  // elements per 16-byte chunk
     double acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0;
@@ -356,7 +439,7 @@ __device__ __forceinline__ void dot_f64_range(const char* xr, const char* w, siz
         for (int i = 0; i < 8; ++i)
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                if constexpr (MODE == MODE_BF16) {
+                if constexpr (mode_bf16(MODE)) {
                     const uint16_t* xs = (const uint16_t*)&xv[u];
                     const uint16_t* ws = (const uint16_t*)&wv[i][u];
 #pragma unroll
@@ -509,10 +592,91 @@ __device__ __forceinline__ void logits_bf16(const RouteArgs& p, float* zs, char*
     }
 }
 
+// Logits of 16 tokens for E <= 8 and d = 1024 * NBAT, without barriers in
+// the copy phase. Wave w owns the chunks [w*cq, w*cq + cq) of the d axis
+// (16-byte chunks, cq = 32 * NBAT), taken in NBAT batches of 8 MFMAs. MFMA u
+// of batch b covers chunks 32b + 4u .. 32b + 4u + 3 of the wave's range,
+// lane group q taking chunk 32b + 4u + q of its token row (A) and of its
+// router row (B): a k permutation that both operands share, under which a
+// token row is read in 64-byte runs per load. The x tile goes straight from
+// global memory into registers (all 8 * NBAT loads of a lane in flight at
+// once); the wave's own columns of W_router (8 rows, rows past E repeat row
+// E - 1) are copied into the wave's own LDS area before them, 4 KB per batch
+// (row r, chunk j at slot 32r + (j ^ r): the eight rows a read phase touches
+// fall in distinct banks), so a wave waits only for its own copies. The four
+// partial tiles are summed in wave order.
+// Batch B of the MFMAs of logits_bf16_res, then the following ones. The copies
+// were issued before every x load: at most 8 * NBAT + 4 * (NBAT - 1 - B)
+// operations in flight means the copies of batches 0..B have landed.
+template <int NBAT, int B = 0>
+__device__ __forceinline__ void res_mfma(const uint4 (&a)[NBAT][8], const char* wv, int nb, int q, f32x4& acc) {
+    wait_vmcnt<8 * NBAT + 4 * (NBAT - 1 - B)>();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const uint4 bv = *(const uint4*)(wv + B * 4096 + (nb * 32 + ((4 * u + q) ^ nb)) * 16);
+        acc = mfma16(a[B][u], bv, acc);
+    }
+    if constexpr (B + 1 < NBAT) res_mfma<NBAT, B + 1>(a, wv, nb, q, acc);
+}
+
+template <int NBAT>
+__device__ __forceinline__ void logits_bf16_res(const RouteArgs& p, float* zs, char* wl, float* part, int t0) {
+    const uint16_t* x = (const uint16_t*)p.x;
+    const uint16_t* w = (const uint16_t*)p.w;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int q = lane >> 4, r16 = lane & 15;
+    const int d = p.d, E = p.E, T = p.T;
+    const int cb = wave * 32 * NBAT;
+    // the bias of this lane's logit column, issued before every copy so that
+    // the waits below cover it
+    const float bz = (p.bias && r16 < E) ? p.bias[r16] : 0.f;
+    char* wv = wl + wave * NBAT * 4096;
+    const uint32_t wv0 = (uint32_t)(uintptr_t)wv;
+    // 1. copies of the wave's router columns: instruction m of batch b fills
+    // LDS rows 2m and 2m + 1 (lane i: row 2m + i / 32, slot i % 32)
+    {
+        const int j = lane & 31;
+#pragma unroll
+        for (int b = 0; b < NBAT; ++b)
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int r = 2 * m + (lane >> 5);
+                const uint16_t* src = w + (size_t)min(r, E - 1) * d + (size_t)(cb + 32 * b + (j ^ r)) * 8;
+                dma16(src, __builtin_amdgcn_readfirstlane(wv0 + (uint32_t)(b * 4096 + m * 1024)));
+            }
+    }
+    // 2. the x tile of this lane: token t0 + r16 (clamped to the last token)
+    const uint16_t* xr = x + (size_t)min(t0 + r16, T - 1) * d + (size_t)(cb + q) * 8;
+    uint4 a[NBAT][8];
+#pragma unroll
+    for (int b = 0; b < NBAT; ++b)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) a[b][u] = *(const uint4*)(xr + (size_t)(32 * b + 4 * u) * 8);
+    // 3. MFMAs, batch by batch; B of lane (q, r16): LDS row r16 & 7
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    res_mfma<NBAT>(a, wv, r16 & 7, q, acc);
+    // 3. partial tiles: D[4q + i][r16] is token 4q + i, expert r16
+    if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) part[((wave - 1) * 16 + 4 * q + i) * 16 + r16] = acc[i];
+    }
+    __syncthreads();
+    if (wave == 0 && r16 < E) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int tl = 4 * q + i;
+            float v = acc[i];
+#pragma unroll
+            for (int kk = 0; kk < 3; ++kk) v += part[(kk * 16 + tl) * 16 + r16];
+            zs[tl * 17 + r16] = v + bz;
+        }
+    }
+}
+
 template <int MODE, int TB, int NBLK, int KW>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     extern __shared__ __align__(16) char smem[];
-    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(p.E);
+    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(p.E, p.d);
     constexpr int BT = 16 * TB;
     constexpr int TPW = BT / 4;  // tokens per wave in the selection steps
     static_assert(TPW * 32 <= 512, "pick area of a wave");
@@ -537,6 +701,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     // ---- 1. logits tile
     if constexpr (MODE == MODE_BF16) {
         logits_bf16<TB, NBLK, KW>(p, zs, ring, dummy, t0);
+    } else if constexpr (MODE == MODE_BF16_RES) {
+        logits_bf16_res<KW>(p, zs, ring, (float*)(ring + res_w_bytes(p.d)), t0);
     } else if constexpr (MODE == MODE_F32) {
         const float* x = (const float*)p.x;
         const float* w = (const float*)p.w;
@@ -598,7 +764,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
         const int nq = q0 + q1 + q2 + q3;
         const int sp = nq >= 3 ? 1 : (nq == 2 ? 2 : 4);  // waves per token
         const int team = wave / sp, mate = wave % sp;
-        const size_t xrow_bytes = (size_t)p.d * (MODE == MODE_BF16 ? 2 : 4);
+        const size_t xrow_bytes = (size_t)p.d * (mode_bf16(MODE) ? 2 : 4);
         const int nch = (int)(xrow_bytes / 16);
         const int qc = ceil_div(nch, sp);
         const int cb = min(nch, mate * qc), ce = min(nch, cb + qc);
@@ -758,7 +924,19 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
                 if (e < E && !cand[j]) so += __expf((float)((double)fz[j] - top));
             }
             so = group_sum<kWave>(so);
-            finish_token<double>(p, t, lane, kWave, pk3, pv3, top, so, true);
+            if (k <= kRegK) {
+                // the pick list into registers (entries past k are never used)
+                int hk[kRegK];
+                double hv[kRegK];
+#pragma unroll
+                for (int j = 0; j < kRegK; ++j) {
+                    hk[j] = pk3[j];
+                    hv[j] = pv3[j];
+                }
+                finish_regs(p, t, lane, kWave, hk, hv, so, true);
+            } else {
+                finish_token<double>(p, t, lane, kWave, pk3, pv3, top, so, true);
+            }
             lds_reads_done();  // cl is rewritten for the next queued token
         }
     }
@@ -766,7 +944,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
 
 template <int MODE, int TB, int NBLK, int KW = 1>
 hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
-    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(a.E);
+    const RouteSmem sm = route_smem<MODE, TB, NBLK, KW>(a.E, a.d);
     auto kern = route_kernel<MODE, TB, NBLK, KW>;
     // the kernel's dynamic LDS limit is raised to the whole 160 KiB once per
     // device (the attribute only permits; each launch asks for what it uses)
@@ -783,6 +961,18 @@ hipError_t launch_one(const RouteArgs& a, hipStream_t s) {
     dim3 grid(ceil_div(a.T, 16 * TB));
     hipLaunchKernelGGL(kern, grid, dim3(kRouteThreads), sm.total(), s, a);
     return hipGetLastError();
+}
+
+// x straight into registers, 16 tokens per workgroup: E <= 8 and d a whole
+// number (at most 4) of 1024-column batches per wave
+bool res_fits(const RouteArgs& a) { return a.E <= 8 && a.d % 1024 == 0 && a.d <= 4096; }
+hipError_t launch_res(const RouteArgs& a, hipStream_t s) {
+    switch (a.d / 1024) {
+        case 1: return launch_one<MODE_BF16_RES, 1, 1, 1>(a, s);
+        case 2: return launch_one<MODE_BF16_RES, 1, 1, 2>(a, s);
+        case 3: return launch_one<MODE_BF16_RES, 1, 1, 3>(a, s);
+        default: return launch_one<MODE_BF16_RES, 1, 1, 4>(a, s);
+    }
 }
 
 template <int TB>
@@ -806,6 +996,7 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
     if (a.T == 0) return hipSuccess;
     if (a.logits_in) return launch_one<MODE_LOGITS_IN, 1, 1>(a, s);
     if (a.dtype == BMOE_F32) return launch_one<MODE_F32, 1, 1>(a, s);
+    if (res_fits(a)) return launch_res(a, s);
     // tokens per workgroup: as many as keep >= 256 workgroups (one per CU), so
     // that W_router (L2-resident) is re-read as few times as possible
     if (a.T >= 64 * 256) return launch_bf16<4>(a, s);

@@ -90,12 +90,14 @@ def test_route_exact(name, seed):
     assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
 
 
-@pytest.mark.parametrize("E,d", [(16, 256), (8, 256), (8, 4096)], ids=["mfma-E16", "valu-E8", "valu-E8-d4096"])
-def test_route_near_ties_decided_in_f64(E, d):
+@pytest.mark.parametrize("E,d,k", [(16, 256, 4), (8, 256, 4), (8, 4096, 4), (16, 256, 10)],
+                         ids=["ring-E16", "ring-E8", "direct-E8-d4096", "ring-E16-k10"])
+def test_route_near_ties_decided_in_f64(E, d, k):
     """Two experts whose logits differ by far less than the fp32 rounding error
-    (and exact ties) are still ordered as float64 orders them (on the MFMA
-    logits path and on the dot-product path of routers with few experts)."""
-    cfg = W.LayerConfig("ties", T=96, d=d, E=E, top_k=4, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
+    (and exact ties) are still ordered as float64 orders them (on the LDS-ring
+    logits path, on the direct path of routers with at most 8 experts, and with
+    more picks than the register pick list holds)."""
+    cfg = W.LayerConfig("ties", T=96, d=d, E=E, top_k=k, G=4, d_ff=64, dtype="bf16", zipf_s=1.0)
     L = W.make_layer(cfg, 5)
     # expert 7's router row equals expert 3's except one bf16 ulp in column 17;
     # column 17 of x is tiny, so the two logits differ by |x[t,17]| * ulp
@@ -118,6 +120,29 @@ def test_route_near_ties_decided_in_f64(E, d):
     torch.cuda.synchronize()
     assert np.array_equal(got["topk_idx"].cpu().numpy(), ref["topk_idx"])
     assert np.array_equal(got["slot_group"].cpu().numpy(), ref["slot_group"])
+    assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
+
+
+@pytest.mark.parametrize("E,d,k,T", [(8, 1024, 2, 300), (8, 2048, 2, 300), (8, 3072, 3, 257), (5, 4096, 2, 300),
+                                     (3, 2048, 1, 40), (8, 4096, 8, 300), (16, 256, 9, 300), (16, 1024, 3, 300)],
+                         ids=["direct-d1024", "direct-d2048", "direct-d3072", "direct-E5", "direct-E3-k1",
+                              "direct-k8", "ring-k9", "ring-E16-d1024"])
+def test_route_shapes(E, d, k, T):
+    """Every bf16 logits path and both pick lists (registers for k <= 8, LDS
+    beyond) on ragged token counts: integers exact, gates to tolerance."""
+    cfg = W.LayerConfig("rshape", T=T, d=d, E=E, top_k=k, G=max(1, E // 2), d_ff=64, dtype="bf16", zipf_s=1.0,
+                        norm_topk=1 if k == 2 else 0)
+    L = W.make_layer(cfg, 3, with_weights=False)
+    ref = oracle.route(L.f32("x"), L.f32("w_router"), L.bias, L.e2g, cfg.top_k, cfg.norm_topk)
+    w = {"w_router": dev_tensor(L.w_router, "bf16"), "bias": torch.from_numpy(L.bias).cuda(),
+         "e2g": torch.from_numpy(L.e2g).cuda()}
+    got = B.route(desc_of(cfg), dev_tensor(L.x, "bf16"), w["w_router"], w["bias"], w["e2g"], want_logits=True)
+    torch.cuda.synchronize()
+    zerr = np.abs(got["logits"].cpu().numpy().astype(np.float64) - ref["logits"]).max()
+    assert zerr < B.ROUTE_RECHECK_GAP / 4, f"fp32 logit error {zerr:.3e}"
+    for key in ("topk_idx", "slot_group"):
+        assert np.array_equal(got[key].cpu().numpy(), ref[key]), key
+    assert_gates(got["topk_w"].cpu().numpy(), ref["topk_w"], "topk_w")
     assert_gates(got["slot_gate"].cpu().numpy(), ref["slot_gate"], "slot_gate")
 
 
