@@ -335,6 +335,17 @@ def time_layer(cfg, args, dev, device_weights=False):
             e1.record()
         torch.cuda.synchronize()
         cold_ms[s] = float(np.median([a.elapsed_time(b) for a, b in evs]))
+    # the same protocol around a one-workgroup elementwise launch: the launch
+    # and event overhead contained in every cold time above
+    tiny = torch.zeros(64, device=dev)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+    for e0, e1 in evs:
+        flush.sum()
+        e0.record()
+        tiny.add_(1.0)
+        e1.record()
+    torch.cuda.synchronize()
+    cold_ms["launch_floor"] = float(np.median([a.elapsed_time(b) for a, b in evs]))
     del flush
     del layer, w, x
     torch.cuda.empty_cache()
@@ -507,7 +518,10 @@ def main():
         "stages": stage_out,
         "stages_note": "us / rates: the stage launched alone back to back (warm: activations, and weights "
                        "below 256 MB, may be served from the 256 MB MALL); in_step_us: inside the timed steps; "
-                       "cold_*: median launch after a 1 GiB read pass that evicts L2 and the MALL",
+                       "cold_*: median launch after a 1 GiB read pass that evicts L2 and the MALL, timed by HIP "
+                       "events around the one launch (so it includes the launch and event overhead that "
+                       "cold_launch_floor_us measures on a one-workgroup elementwise launch)",
+        "cold_launch_floor_us": round(cold_ms["launch_floor"] * 1e3, 2),
         "cpu_baseline": None,
     }
 

@@ -44,8 +44,17 @@ static_assert(BMOE_MAX_EXPERTS <= kRouteThreads, "one map entry per thread");
 // MODE_BF16: x and W_router through the LDS ring; MODE_BF16_RES: x straight
 // into registers, each wave's columns of W_router in its own LDS area (E <= 8,
 // d = 1024 * NBAT, NBAT <= 4)
-enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2, MODE_BF16_RES = 3 };
-__host__ __device__ constexpr bool mode_bf16(int mode) { return mode == MODE_BF16 || mode == MODE_BF16_RES; }
+// MODE_BF16_XD: 32 tokens, 17..64 experts, d = 64 * NU (NU in 8, 16, 32): x
+// straight into registers, W_router alone through an LDS ring
+enum { MODE_LOGITS_IN = 0, MODE_F32 = 1, MODE_BF16 = 2, MODE_BF16_RES = 3, MODE_BF16_XD = 4 };
+__host__ __device__ constexpr bool mode_bf16(int mode) { return mode >= MODE_BF16; }
+
+// KW of MODE_BF16_XD carries NU (k-steps of 32 columns per wave, low 6 bits)
+// and NS (ring slots, the bits above)
+__host__ __device__ constexpr int xd_nu(int kw) { return kw & 63; }
+__host__ __device__ constexpr int xd_ns(int kw) { return kw >> 6; }
+constexpr int kXdSlot = 16 * 1024;        // 64 router rows x 2 column halves x 64 columns, bf16
+constexpr int kXdPart = 2 * 16 * 64 * 4;  // partial tiles of the waves of the second half
 
 // LDS of the router columns (8 rows of d, four wave areas) and of the
 // partial logit tiles of waves 1..3
@@ -93,10 +102,11 @@ __host__ __device__ inline RouteSmem route_smem(int E, int d) {
     s.zs_bytes = ((size_t)bt * s.zstride * 4 + 15) / 16 * 16;
     s.flag_bytes = 2048;
     s.cand_bytes = 4 * 2048;
-    s.dummy_bytes = (MODE == MODE_BF16) ? 4 * 1024 : 0;
+    s.dummy_bytes = (MODE == MODE_BF16 || MODE == MODE_BF16_XD) ? 4 * 1024 : 0;
     s.ring_bytes = 0;
     if constexpr (MODE == MODE_BF16) s.ring_bytes = (size_t)RouteCfg<TB, NBLK, KW>::NSLOT * RouteCfg<TB, NBLK, KW>::SLOT;
     if constexpr (MODE == MODE_BF16_RES) s.ring_bytes = res_w_bytes(d) + kResPartBytes;
+    if constexpr (MODE == MODE_BF16_XD) s.ring_bytes = (size_t)xd_ns(KW) * kXdSlot + kXdPart;
     return s;
 }
 
@@ -673,6 +683,114 @@ __device__ __forceinline__ void logits_bf16_res(const RouteArgs& p, float* zs, c
     }
 }
 
+// Logits of 32 tokens for 17..64 experts and d = 64 * NU. Wave w takes token
+// block tb = w & 1 (16 tokens) and column half h = w >> 1; k-step u of a wave
+// covers chunks 4u .. 4u + 3 of its half (16-byte chunks), lane group q taking
+// chunk 4u + q of its token row (A) and of the router rows (B). The x tile
+// goes straight into registers (NU loads per lane, all issued at once, after
+// the first NS - 1 router slots); W_router alone streams through a ring of NS
+// slots shared by the four waves, a slot holding 64 columns of each half of
+// all 64 (padded) router rows: rows past E repeat row E - 1, slot row
+// R = 64 h + e, its 8 chunks at positions chunk ^ (e & 7). The compiler waits
+// for the whole x tile before the ring loop (a wait for one x load inside it
+// would also wait for every copy issued after that load). The halves' partial
+// tiles are summed in a fixed order.
+template <int NU, int NS>
+__device__ __forceinline__ void logits_bf16_xd(const RouteArgs& p, float* zs, char* ring, char* dummy, float* part,
+                                               int t0) {
+    constexpr int NSTEP = NU / 2;  // 64 columns of each half per ring step
+    static_assert(NSTEP >= 1 && NS >= 2 && NS <= 8, "ring shape");
+    const uint16_t* x = (const uint16_t*)p.x;
+    const uint16_t* w = (const uint16_t*)p.w;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int q = lane >> 4, r16 = lane & 15;
+    const int tb = wave & 1, h = wave >> 1;
+    const int d = p.d, E = p.E, T = p.T;
+    const int nchh = 4 * NU;  // chunks per half row
+    float bz[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int e = nb * 16 + r16;
+        bz[nb] = (p.bias && e < E) ? p.bias[e] : 0.f;
+    }
+    // copy instruction i = wave + 4j of a slot fills slot rows 8i .. 8i + 7
+    // (lane: row 8i + lane / 8, position lane % 8); step c adds 64 columns
+    const uint16_t* wsrc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int R = 8 * (wave + 4 * j) + (lane >> 3);
+        const int hh = R >> 6, e = R & 63;
+        wsrc[j] = w + (size_t)min(e, E - 1) * d + (size_t)(hh * nchh + ((lane & 7) ^ (e & 7))) * 8;
+    }
+    // every workgroup of an XCD (workgroups are dealt to the 8 XCDs in turn)
+    // first pulls its 1/32 share of W_router into that XCD's L2 (copies into
+    // the wave's dummy area), so that the ring's copies hit in L2 instead of
+    // all waiting on the same HBM misses step after step
+    {
+        const size_t wbytes = (size_t)E * d * 2;
+        const size_t share = (wbytes / 32 + 4095) / 4096 * 4096;
+        const size_t o0 = (size_t)((blockIdx.x >> 3) & 31) * share + (size_t)wave * (share / 4);
+        const uint32_t dm = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dummy + wave * 1024);
+        for (size_t o = o0; o < o0 + share / 4 && o < wbytes; o += 1024)
+            dma16((const char*)w + min(o + (size_t)lane * 16, wbytes - 16), dm);
+    }
+    const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
+    auto issue = [&](int c, int slot) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            dma16(wsrc[j] + c * 64,
+                  __builtin_amdgcn_readfirstlane(ring0 + (uint32_t)(slot * kXdSlot + (wave + 4 * j) * 1024)));
+    };
+#pragma unroll
+    for (int c = 0; c < NS - 1; ++c)
+        if (c < NSTEP) issue(c, c);
+    const uint16_t* xr = x + (size_t)min(t0 + 16 * tb + r16, T - 1) * d + (size_t)(h * nchh + q) * 8;
+    uint4 a[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) a[u] = *(const uint4*)(xr + u * 32);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) asm volatile("" ::"v"(a[u].x), "v"(a[u].y), "v"(a[u].z), "v"(a[u].w));
+    f32x4 acc[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NSTEP; ++c) {
+        // copies issued so far: steps 0 .. min(NSTEP - 1, c + NS - 2)
+        wait_vmcnt_rt<4>(min(NSTEP - 1 - c, NS - 2));
+        wg_barrier();
+        // the slot read in the previous step is free for step c + NS - 1
+        if (c + NS - 1 < NSTEP) issue(c + NS - 1, (c + NS - 1) % NS);
+        const char* base = ring + (c % NS) * kXdSlot;
+#pragma unroll
+        for (int uu = 0; uu < 2; ++uu) {
+            const int j = 4 * uu + q;
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                const int e = nb * 16 + r16;
+                const uint4 bv = *(const uint4*)(base + ((h * 64 + e) * 8 + (j ^ (e & 7))) * 16);
+                acc[nb] = mfma16(a[2 * c + uu], bv, acc[nb]);
+            }
+        }
+    }
+    // D[4q + i][r16] of block nb: token 16 tb + 4q + i, expert 16 nb + r16
+    if (h == 1) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) part[(tb * 16 + 4 * q + i) * 64 + nb * 16 + r16] = acc[nb][i];
+    }
+    __syncthreads();
+    if (h == 0) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int tl = tb * 16 + 4 * q + i, e = nb * 16 + r16;
+                if (e < E) zs[tl * 65 + e] = acc[nb][i] + part[tl * 64 + e] + bz[nb];
+            }
+    }
+}
+
 template <int MODE, int TB, int NBLK, int KW>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
     extern __shared__ __align__(16) char smem[];
@@ -703,6 +821,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs p) {
         logits_bf16<TB, NBLK, KW>(p, zs, ring, dummy, t0);
     } else if constexpr (MODE == MODE_BF16_RES) {
         logits_bf16_res<KW>(p, zs, ring, (float*)(ring + res_w_bytes(p.d)), t0);
+    } else if constexpr (MODE == MODE_BF16_XD) {
+        logits_bf16_xd<xd_nu(KW), xd_ns(KW)>(p, zs, ring, dummy, (float*)(ring + xd_ns(KW) * kXdSlot), t0);
     } else if constexpr (MODE == MODE_F32) {
         const float* x = (const float*)p.x;
         const float* w = (const float*)p.w;
@@ -975,6 +1095,23 @@ hipError_t launch_res(const RouteArgs& a, hipStream_t s) {
     }
 }
 
+// x straight into registers, W_router alone through the ring: 17..64 experts,
+// d of 512, 1024 or 2048 columns, at least 4096 tokens (128 workgroups of 32
+// tokens); more than 256 workgroups run two per CU, with three slots each
+bool xd_fits(const RouteArgs& a) {
+    return a.E > 16 && a.E <= 64 && (a.d == 512 || a.d == 1024 || a.d == 2048) && a.T >= 4096;
+}
+template <int NU>
+hipError_t launch_xd_nu(const RouteArgs& a, hipStream_t s) {
+    if (ceil_div(a.T, 32) > 256) return launch_one<MODE_BF16_XD, 2, 4, NU + 64 * 3>(a, s);
+    return launch_one<MODE_BF16_XD, 2, 4, NU + 64 * 6>(a, s);
+}
+hipError_t launch_xd(const RouteArgs& a, hipStream_t s) {
+    if (a.d == 2048) return launch_xd_nu<32>(a, s);
+    if (a.d == 1024) return launch_xd_nu<16>(a, s);
+    return launch_xd_nu<8>(a, s);
+}
+
 template <int TB>
 hipError_t launch_bf16(const RouteArgs& a, hipStream_t s) {
     // two 64-column units per wave and copy step where two ring slots still
@@ -997,6 +1134,7 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
     if (a.logits_in) return launch_one<MODE_LOGITS_IN, 1, 1>(a, s);
     if (a.dtype == BMOE_F32) return launch_one<MODE_F32, 1, 1>(a, s);
     if (res_fits(a)) return launch_res(a, s);
+    if (xd_fits(a)) return launch_xd(a, s);
     // tokens per workgroup: as many as keep >= 256 workgroups (one per CU), so
     // that W_router (L2-resident) is re-read as few times as possible
     if (a.T >= 64 * 256) return launch_bf16<4>(a, s);
