@@ -196,7 +196,9 @@ BMOE_API bmoe_status brownout_moe_route(const bmoe_desc* desc, const void* x, co
  * offsets[G] = -1 (the sentinel to check), every slot_row -1, no row copied;
  * the FFN and combine then see no rows. It still leaves the workspace zero.
  * Implementation: a histogram with LDS atomics and a single-pass decoupled
- * look-back scan across token tiles, then a 128-bit row gather.
+ * look-back scan across token tiles, then a 128-bit row gather; at most 256
+ * tokens (one tile) take one kernel in which every workgroup rebuilds the
+ * tile's histogram and prefix in LDS before gathering its tokens' rows.
  */
 BMOE_API bmoe_status brownout_moe_dispatch(const bmoe_desc* desc, const int32_t* slot_group,
                                   const void* x, int32_t* counts, int32_t* offsets,

@@ -16,6 +16,7 @@
 // Kernel 2 (permute), one wave per token: adds offsets[group] to the relative
 // row, writes perm_token, and copies x[t] into each of its rows with 128-bit
 // loads and stores. Workgroup 0 clears the look-back state for the next call.
+// At most 256 tokens (one tile) take a single kernel that does both.
 #include <algorithm>
 #include <mutex>
 
@@ -315,6 +316,120 @@ __global__ __launch_bounds__(256) void permute_index_kernel(const int32_t* __res
     slot_row[o] = row;
 }
 
+// Dispatch of at most one tile of tokens (T <= 256) in one kernel: every
+// workgroup rebuilds the tile's per-group token masks and their prefix in
+// LDS (a few hundred slots), so no workgroup waits on another and the
+// histogram kernel's launch is saved; workgroup w then takes tokens
+// 4w .. 4w+3, one wave each, as the permute kernel does. The workspace is
+// only read: a ticket left set by a call cut short gives the "no rows"
+// result of the two-kernel path, and the last workgroup to finish (counted
+// in `done`, after every workgroup has read the ticket) clears it.
+template <int VEC>
+__global__ __launch_bounds__(256) void dispatch_small_kernel(const int32_t* __restrict__ slot_group,
+                                                             int32_t* __restrict__ slot_row,
+                                                             int32_t* __restrict__ counts,
+                                                             int32_t* __restrict__ offsets,
+                                                             int32_t* __restrict__ perm_token,
+                                                             const uint4* __restrict__ x, uint4* __restrict__ x_perm,
+                                                             void* ws, int T, int k, int G, int nch, int rows_cap) {
+    __shared__ unsigned long long masks[BMOE_MAX_EXPERTS][kTile / 64];
+    __shared__ int s_off[BMOE_MAX_EXPERTS];
+    __shared__ int s_scan[256];
+    DispatchWs* hdr = (DispatchWs*)ws;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t = blockIdx.x * 4 + wave;  // this wave's token
+    const bool stale = __hip_atomic_load(&hdr->ticket, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+    if (stale) {
+        if (blockIdx.x == 0) {
+            for (int g = tid; g <= G; g += 256) {
+                if (g < G) counts[g] = 0;
+                offsets[g] = g < G ? 0 : -1;
+            }
+        }
+        if (t < T && lane < k) slot_row[(size_t)t * k + lane] = -1;
+        __syncthreads();  // every wave of this workgroup has read the ticket
+        if (tid == 0) {
+            __threadfence();
+            if (atomicAdd(&hdr->done, 1) == (int)gridDim.x - 1) {
+                uint64_t* status = (uint64_t*)((char*)ws + sizeof(DispatchWs));
+                for (int g = 0; g < G; ++g) status[g] = 0ull;
+                __hip_atomic_store(&hdr->ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&hdr->err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&hdr->done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        return;
+    }
+    for (int g = tid; g < G; g += 256) {
+#pragma unroll
+        for (int w = 0; w < kTile / 64; ++w) masks[g][w] = 0ull;
+    }
+    __syncthreads();
+    // thread tid sets the bit of token tid in the mask of each of its groups
+    if (tid < T) {
+        for (int i = 0; i < k; ++i) {
+            const int g = slot_group[(size_t)tid * k + i];
+            if (g >= 0 && g < G) atomicOr(&masks[g][tid >> 6], 1ull << (tid & 63));
+        }
+    }
+    __syncthreads();
+    int c = 0;
+    if (tid < G) {
+#pragma unroll
+        for (int w = 0; w < kTile / 64; ++w) c += __popcll(masks[tid][w]);
+    }
+    int sum;
+    const int ex = block_exclusive_scan_256(c, s_scan, &sum);
+    if (tid < G) {
+        s_off[tid] = ex;
+        if (blockIdx.x == 0) {
+            counts[tid] = c;
+            offsets[tid] = ex;
+        }
+    }
+    if (blockIdx.x == 0 && tid == 0) offsets[G] = sum;
+    __syncthreads();
+    if (t >= T) return;
+    int row = -1;
+    if (lane < k) {
+        const size_t o = (size_t)t * k + lane;
+        const int g = slot_group[o];
+        if (g >= 0 && g < G) {
+            const int w = t >> 6;
+            int rank = __popcll(masks[g][w] & ((1ull << (t & 63)) - 1ull));
+            for (int ww = 0; ww < w; ++ww) rank += __popcll(masks[g][ww]);
+            row = s_off[g] + rank;
+            if (row < 0 || row >= rows_cap) row = -1;
+            else perm_token[row] = t;
+        }
+        slot_row[o] = row;
+    }
+    if (x_perm == nullptr) return;
+    const uint4* src = x + (size_t)t * nch;
+    int rows[BMOE_MAX_TOPK];
+#pragma unroll
+    for (int i = 0; i < BMOE_MAX_TOPK; ++i) rows[i] = i < k ? __shfl(row, i) : -1;
+    for (int c0 = lane; c0 < nch; c0 += 64 * VEC) {
+        uint4 v[VEC];
+#pragma unroll
+        for (int u = 0; u < VEC; ++u) {
+            const int cc = c0 + 64 * u;
+            v[u] = src[cc < nch ? cc : 0];
+        }
+#pragma unroll
+        for (int i = 0; i < BMOE_MAX_TOPK; ++i) {
+            if (rows[i] >= 0) {
+                uint4* dst = x_perm + (size_t)rows[i] * nch;
+#pragma unroll
+                for (int u = 0; u < VEC; ++u) {
+                    const int cc = c0 + 64 * u;
+                    if (cc < nch) store_stream(dst + cc, v[u]);
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 size_t dispatch_ws_bytes(int T, int G) {
@@ -331,6 +446,19 @@ static hipError_t clear_ws(void* ws, size_t bytes, hipStream_t s) {
 
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
     if (a.T == 0) return hipSuccess;
+    if (a.T <= kTile) {
+        // one tile: a single kernel (no look-back, no second launch)
+        const int nch = a.x_perm ? a.d * a.elem_bytes / 16 : 0;
+        if (nch > 256)
+            hipLaunchKernelGGL(dispatch_small_kernel<8>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                               a.slot_row, a.counts, a.offsets, a.perm_token, (const uint4*)a.x,
+                               (uint4*)a.x_perm, a.ws, a.T, a.k, a.G, nch, a.T * a.k);
+        else
+            hipLaunchKernelGGL(dispatch_small_kernel<4>, dim3(ceil_div(a.T, 4)), dim3(256), 0, s, a.slot_group,
+                               a.slot_row, a.counts, a.offsets, a.perm_token, (const uint4*)a.x,
+                               (uint4*)a.x_perm, a.ws, a.T, a.k, a.G, nch, a.T * a.k);
+        return hipGetLastError();
+    }
     const int ntiles = ceil_div(a.T, kTile);
     hipLaunchKernelGGL(hist_scan_kernel, dim3(ntiles), dim3(kTile), 0, s, a.slot_group, a.slot_row,
                        a.counts, a.offsets, a.ws, a.T, a.k, a.G, ntiles);

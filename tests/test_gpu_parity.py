@@ -124,9 +124,12 @@ def test_route_near_ties_decided_in_f64(E, d, k):
 
 
 @pytest.mark.parametrize("E,d,k,T", [(8, 1024, 2, 300), (8, 2048, 2, 300), (8, 3072, 3, 257), (5, 4096, 2, 300),
-                                     (3, 2048, 1, 40), (8, 4096, 8, 300), (16, 256, 9, 300), (16, 1024, 3, 300)],
+                                     (3, 2048, 1, 40), (8, 4096, 8, 300), (16, 256, 9, 300), (16, 1024, 3, 300),
+                                     (17, 512, 3, 4100), (33, 1024, 5, 4111), (64, 2048, 6, 8200),
+                                     (60, 2048, 9, 4096)],
                          ids=["direct-d1024", "direct-d2048", "direct-d3072", "direct-E5", "direct-E3-k1",
-                              "direct-k8", "ring-k9", "ring-E16-d1024"])
+                              "direct-k8", "ring-k9", "ring-E16-d1024", "xdirect-E17-d512", "xdirect-E33-d1024",
+                              "xdirect-2perCU", "xdirect-k9"])
 def test_route_shapes(E, d, k, T):
     """Every bf16 logits path and both pick lists (registers for k <= 8, LDS
     beyond) on ragged token counts: integers exact, gates to tolerance."""
@@ -171,13 +174,15 @@ def test_dispatch_exact(name, seed):
     assert int(ws.count_nonzero()) == 0, "dispatch must leave its workspace all zero"
 
 
-def test_dispatch_reports_a_dirty_workspace():
+@pytest.mark.parametrize("name", ["fine-s", "decode"], ids=["two-kernels", "one-tile"])
+def test_dispatch_reports_a_dirty_workspace(name):
     """A workspace left with a stale tile ticket (as a call cut short between
     its two kernels would leave it): the call writes the "no rows" result
     with offsets[G] = -1 instead of stale or partial rows, leaves the
-    workspace zero, and the next call is correct. Every kernel exits
-    normally (the stale tickets are past the tile count)."""
-    L, ref = case("fine-s", 0)
+    workspace zero, and the next call is correct; on the histogram +
+    permute path and on the one-kernel path of at most 256 tokens. Every
+    kernel exits normally (the stale tickets are past the tile count)."""
+    L, ref = case(name, 0)
     cfg = L.cfg
     desc = desc_of(cfg)
     sg = torch.from_numpy(ref["slot_group"]).cuda()
