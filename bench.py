@@ -105,6 +105,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip timing the step captured into a HIP graph (graph_ms_per_step)")
     ap.add_argument("--no-compare-ungrouped", action="store_true",
                     help="skip timing the same layer with no grouping (G = E, every expert its own group: "
                          "zero brownout) and the speedup of grouping")
@@ -159,6 +161,35 @@ def device_ffn_weights(cfg, seed, dev):
         fs = cfg.d_ff_shared
         w.update(w_gate_sh=draw((1, fs, d)), w_up_sh=draw((1, fs, d)), w_down_sh=draw((1, d, fs)))
     return w
+
+
+def graph_step_ms(step, reps):
+    """Wall-clock ms per replay of one step captured into a HIP graph (None,
+    with a note on stderr, if the capture fails)."""
+    import torch
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            g.replay()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / reps
+        del g
+        return ms
+    except RuntimeError as e:
+        print(f"[bench] graph capture failed: {e}", file=sys.stderr, flush=True)
+        torch.cuda.synchronize()
+        return None
 
 
 def time_layer(cfg, args, dev, device_weights=False):
@@ -274,6 +305,11 @@ def time_layer(cfg, args, dev, device_weights=False):
     torch.cuda.synchronize()
     per_stage_ms = {s: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
                     for i, s in enumerate(stages)}
+    # the same step captured once into a HIP graph and replayed: the steps'
+    # kernels without the host's launch work (wall clock over the replays)
+    graph_ms = None
+    if not getattr(args, "no_graph", False):
+        graph_ms = graph_step_ms(step, args.steps)
     # each stage alone, launched back to back (the in-step events above also
     # hold the gaps between kernels, which dominate the short stages)
     iso_ms = {}
@@ -349,7 +385,7 @@ def time_layer(cfg, args, dev, device_weights=False):
     del flush
     del layer, w, x
     torch.cuda.empty_cache()
-    return L0, (cfg, seg_info, ep_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
+    return L0, (cfg, seg_info, ep_ms, graph_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
 
 
 def ungrouped_line(cfg, args, dev, ms_grouped):
@@ -422,7 +458,7 @@ def main():
     torch.cuda.set_device(dev)
     B.load_library()
     cfg0 = cfg
-    L, (cfg, seg_info, ep_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = \
+    L, (cfg, seg_info, ep_ms, graph_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = \
         time_layer(cfg, args, dev)
     share = parse_share(args.share)
 
@@ -522,6 +558,10 @@ def main():
                        "events around the one launch (so it includes the launch and event overhead that "
                        "cold_launch_floor_us measures on a one-workgroup elementwise launch)",
         "cold_launch_floor_us": round(cold_ms["launch_floor"] * 1e3, 2),
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
+        "graph_note": "one step captured into a HIP graph and replayed `steps` times back to back (wall clock): "
+                      "the kernels without the host's per-call launch work; value and ms_per_step are the eager "
+                      "steps",
         "cpu_baseline": None,
     }
 
@@ -587,10 +627,11 @@ def main():
         for name in ("fine", "heavy", "decode"):
             wcfg = W.CONFIGS[name]
             xargs = argparse.Namespace(**{**vars(args), "share": None, "fused_gather": False})
-            _, _, ms_w, dom_w, _, iso_w, cold_w, N_w, counts_w, _ = time_layer(wcfg, xargs, dev,
-                                                                                 device_weights=True)
+            _, (_, _, _, graph_w), ms_w, dom_w, _, iso_w, cold_w, N_w, counts_w, _ = \
+                time_layer(wcfg, xargs, dev, device_weights=True)
             line = {"workload": WORKLOAD_TEXT[name], "value": round(wcfg.T / (ms_w * 1e-3), 1),
-                    "unit": "tokens/s", "ms_per_step": round(ms_w, 4), "rows_N": N_w,
+                    "unit": "tokens/s", "ms_per_step": round(ms_w, 4),
+                    "graph_ms_per_step": None if graph_w is None else round(graph_w, 4), "rows_N": N_w,
                     "dominant": dominant_rate(wcfg, N_w, counts_w, dom_w, cold_w["ffn_gate_up"]),
                     "stages_us": {k: round(v * 1e3, 2) for k, v in iso_w.items()},
                     "stages_cold_us": {k: round(v * 1e3, 2) for k, v in cold_w.items()}}
