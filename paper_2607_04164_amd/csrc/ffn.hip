@@ -595,14 +595,22 @@ __device__ __forceinline__ void ksteps_prologue(const DmaSrc<C>& src, char* smem
 enum { kAfterNone = 0, kAfterStores = 1 };
 
 // K-steps [ka, kb) of one tile into acc (which the caller zeroed), after
-// ksteps_prologue. Ends with every copy complete and a barrier, so the LDS
-// ring may be reused.
-template <class C>
-__device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], const DmaSrc<C>& src,
-                                            char* smem, int ka, int kb, int wave, int lane, int after) {
+// their first two K-steps' copies were issued (ksteps_prologue, or the
+// previous item's last K-steps). K-step kt lives in ring slot (kt + s0) & 1.
+// The next item (tile tc2, K-steps [nka, nkb); nka == nkb: none) has its
+// first two K-steps copied as if they continued this item's: once this
+// item's own copies are all issued, src is set to the next item's sources
+// and its K-steps nka and nka+1 go into the slots this item's last two
+// K-steps free, so they arrive while this item's results go out (an item of
+// one K-step copies the next item's first K-step after its loop). Ends with
+// a barrier; src then holds the next item's sources.
+template <class C, bool GATED>
+__device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB], DmaSrc<C>& src, char* smem,
+                                            int ka, int kb, int wave, int lane, int after, int s0,
+                                            const GemmParams& p, const TileCoord& tc2, int nka, int nkb) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
     const int wm = wave >> 1, wn = wave & 1;
-    const int n = kb - ka;
+    const int n = kb - ka, nn = nkb - nka;
     // wait for K-step ka: vector-memory operations complete in issue order, so
     // at most (its successors) may still be outstanding
     if (after == kAfterNone && n > 1) wait_vmcnt<C::DMA_PER_STAGE>();
@@ -622,41 +630,59 @@ __device__ __forceinline__ void tile_ksteps(f32x16 (&acc)[C::NMAT][C::MB][C::NB]
     // slot; sub-steps 1-3 issue the copies of K-step kt+2 (6, 5, 5); after
     // sub-step 2 a wait for this wave's older copies and a second barrier
     // make K-step kt+1 resident; sub-step 3 reads its sub-steps 0 and 1.
-    dma_frags<C>(af[0], bf[0], smem, wm, wn, lane, 0);
-    dma_frags<C>(af[1], bf[1], smem, wm, wn, lane, 1);
-    auto kstep = [&](int kt, auto with_dma) {
+    dma_frags<C>(af[0], bf[0], smem + (s0 & 1) * C::STAGE, wm, wn, lane, 0);
+    dma_frags<C>(af[1], bf[1], smem + (s0 & 1) * C::STAGE, wm, wn, lane, 1);
+    // K-step kt; with DMA, the copies of K-step kbyte / (BK * 2) of src go
+    // into its slot once the slot is free
+    auto kstep = [&](int kt, auto with_dma, int kbyte) {
+        const DmaSrc<C>& cs = src;
         constexpr bool DMA = decltype(with_dma)::value;
-        const int slot = kt & 1;
+        const int slot = (kt + s0) & 1;
         const char* cur = smem + slot * C::STAGE;
         const char* nxt = smem + (slot ^ 1) * C::STAGE;
         const uint32_t dma_lds = lds0 + slot * C::STAGE;
-        const int kb = (ka + kt + 2) * C::BK * 2;
+        const int kb = kbyte;
         constexpr int D1 = 6, D2 = 5, D3 = C::DMA_PER_STAGE - D1 - D2;
         __builtin_amdgcn_sched_barrier(0);
-        mfmas_ops<C, 2, 0>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, src,
+        mfmas_ops<C, 2, 0>(acc, af[0], bf[0], af[2], bf[2], cur, 2, af[3], bf[3], cur, 3, wm, wn, lane, cs,
                            dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
         lds_reads_done();
         wg_barrier();  // the slot is free
         __builtin_amdgcn_sched_barrier(0);
         mfmas_ops<C, 0, DMA ? D1 : 0>(acc, af[1], bf[1], af[1], bf[1], cur, 0, af[1], bf[1], cur, 0, wm, wn, lane,
-                                      src, dma_lds, wave, kb, 0);
+                                      cs, dma_lds, wave, kb, 0);
         __builtin_amdgcn_sched_barrier(0);
         mfmas_ops<C, 0, DMA ? D2 : 0>(acc, af[2], bf[2], af[2], bf[2], cur, 0, af[2], bf[2], cur, 0, wm, wn, lane,
-                                      src, dma_lds, wave, kb, D1);
+                                      cs, dma_lds, wave, kb, D1);
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (DMA) wait_vmcnt<D1 + D2>();
         else wait_vmcnt<0>();
         wg_barrier();  // the next K-step is resident
         __builtin_amdgcn_sched_barrier(0);
         mfmas_ops<C, 2, DMA ? D3 : 0>(acc, af[3], bf[3], af[0], bf[0], nxt, 0, af[1], bf[1], nxt, 1, wm, wn, lane,
-                                      src, dma_lds, wave, kb, D1 + D2);
+                                      cs, dma_lds, wave, kb, D1 + D2);
         __builtin_amdgcn_sched_barrier(0);
     };
     int kt = 0;
-    for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{});
-    for (; kt < n; ++kt) kstep(kt, std::false_type{});
+    for (; kt + 2 < n; ++kt) kstep(kt, std::true_type{}, (ka + kt + 2) * C::BK * 2);
+    // this item's copies are all issued: the last two K-steps copy K-steps
+    // j = kt + 2 - n of the next item; where it has no such K-step (or there
+    // is no next item) they copy one it (or this item) has into the free
+    // slot, which nothing reads (one code path, no branch between K-steps)
+    if (nn > 0) dma_sources<C, GATED>(src, p, tc2, wave, lane);
+    for (; kt < n; ++kt) {
+        const int j = kt + 2 - n;
+        const int kj = nn > 0 ? nka + min(j, nn - 1) : ka;
+        kstep(kt, std::true_type{}, kj * C::BK * 2);
+    }
+    // no next item: the last copies (into free slots) complete before the
+    // workgroup can end, so none lands in a later workgroup's LDS
+    if (nn == 0) wait_vmcnt<0>();
     __syncthreads();
+    // an item of one K-step issued only the next item's second K-step: its
+    // first goes in now (the ring is free after the barrier)
+    if (n == 1 && nn > 0) dma_stage<C>(src, lds0 + ((n + s0) & 1) * C::STAGE, wave, nka * C::BK * 2);
 }
 
 template <class C>
@@ -817,18 +843,38 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[C::NMAT][C::MB][C
         for (int h = 0; h < 2; ++h) {
             // rows 16h .. 16h+15 of the 32-row block: accumulator elements 8h .. 8h+7
             __builtin_amdgcn_sched_barrier(0);
+            // the half block's values first, each step over all of them, so
+            // the SiLU chains (exp, add, reciprocal, products) of different
+            // elements overlap instead of running one after another
+            float v[C::NB][8];
+#pragma unroll
+            for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[nb][e] = acc_read(acc[0][mb][nb][8 * h + e]);
+            if constexpr (GATED) {
+                float u[C::NB][8], t[C::NB][8];
+#pragma unroll
+                for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) u[nb][e] = acc_read(acc[1][mb][nb][8 * h + e]);
+#pragma unroll
+                for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) t[nb][e] = __expf(-v[nb][e]);
+#pragma unroll
+                for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) t[nb][e] = __builtin_amdgcn_rcpf(1.f + t[nb][e]);
+#pragma unroll
+                for (int nb = 0; nb < C::NB; ++nb)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[nb][e] = v[nb][e] * t[nb][e] * u[nb][e];
+            }
 #pragma unroll
             for (int nb = 0; nb < C::NB; ++nb)
 #pragma unroll
                 for (int i = 8 * h; i < 8 * h + 8; i += 2) {
-                    float v0, v1;
-                    if constexpr (GATED) {
-                        v0 = silu_mul(acc_read(acc[0][mb][nb][i]), acc_read(acc[1][mb][nb][i]));
-                        v1 = silu_mul(acc_read(acc[0][mb][nb][i + 1]), acc_read(acc[1][mb][nb][i + 1]));
-                    } else {
-                        v0 = acc_read(acc[0][mb][nb][i]);
-                        v1 = acc_read(acc[0][mb][nb][i + 1]);
-                    }
+                    const float v0 = v[nb][i - 8 * h], v1 = v[nb][i + 1 - 8 * h];
                     const uint32_t pk = pack_bf16x2_hw(v0, v1);
                     const int r = 8 * ((i >> 2) - 2 * h) + 4 * (lane >> 5) + (i & 3);
                     const int c = nb * 32 + l32;
@@ -908,7 +954,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
         dma_sources<C, GATED>(src, p, tc, wave, lane);
         zero_acc<C>(acc);
         ksteps_prologue<C>(src, smem, 0, nk, wave);
-        tile_ksteps<C>(acc, src, smem, 0, nk, wave, lane, kAfterNone);
+        tile_ksteps<C, GATED>(acc, src, smem, 0, nk, wave, lane, kAfterNone, 0, p, tc, 0, 0);
         store_tile<C, GATED, FOLD>(acc, p, tc, smem, wave, lane);
     } else {
         const int P = gridDim.x;
@@ -940,8 +986,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             }
             L = -1;
         };
-        // The next item's first copies are issued before this item's results
-        // go out, so they land while the epilogue runs.
+        // The next item's first two K-steps are copied during this item's
+        // last two (tile_ksteps), so they land while this item's results go
+        // out and the pipeline does not drain between items.
         int L, ka, kb, slot;
         next_item(L, ka, kb, slot);
         TileCoord tc;
@@ -950,21 +997,18 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
             dma_sources<C, GATED>(src, p, tc, wave, lane);
             ksteps_prologue<C>(src, smem, ka, kb, wave);
         }
-        int after = kAfterNone;
+        int after = kAfterNone, s0 = 0;
         while (L >= 0) {
             zero_acc<C>(acc);
-            tile_ksteps<C>(acc, src, smem, ka, kb, wave, lane, after);
             int L2, ka2, kb2, slot2;
             next_item(L2, ka2, kb2, slot2);
-            TileCoord tc2;
-            if (L2 >= 0) {
-                tc2 = tile_coord(ts, p.n_seg, L2, C::BM, C::BN);
-                dma_sources<C, GATED>(src, p, tc2, wave, lane);
-                ksteps_prologue<C>(src, smem, ka2, kb2, wave);
-            }
+            TileCoord tc2 = tc;
+            if (L2 >= 0) tc2 = tile_coord(ts, p.n_seg, L2, C::BM, C::BN);
+            tile_ksteps<C, GATED>(acc, src, smem, ka, kb, wave, lane, after, s0, p, tc2, ka2, L2 >= 0 ? kb2 : ka2);
             store_tile<C, GATED, FOLD>(acc, p, tc, smem, wave, lane,
                                        slot < 0 ? nullptr : ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
             after = kAfterStores;
+            s0 = (s0 + kb - ka) & 1;
             L = L2;
             ka = ka2;
             kb = kb2;
