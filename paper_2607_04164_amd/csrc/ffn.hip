@@ -1019,105 +1019,94 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm_dma_kernel(GemmP
 }
 
 // Sums the pieces of every tile that the stream-K split cut, in K order,
-// then applies the epilogue. Workgroup (qs, b) looks at the share boundary
-// b*share; the first boundary inside a tile owns that tile, and qs picks one
-// of kFixSplit slices of the tile's accumulator slots, so a split tile is
-// finished by kFixSplit workgroups at once (one per tile streamed its pieces
-// through a single CU). Each thread adds its float4 slots of the pieces in
-// the order of the pieces, as the unsplit path would, and writes its four
-// rows of one column straight to the output.
-constexpr int kFixSplit = 16;
+// then applies the epilogue. P persistent workgroups take the work items
+// (split tile, slice) in turn: a tile of the split range is split when a
+// share boundary falls strictly inside it, and a slice is one of kFixSplit
+// parts of the tile's accumulator slots, so a split tile is finished by
+// kFixSplit workgroups at once. Each thread adds its float4 slots of the
+// pieces in the order of the pieces, as the unsplit path would (eight
+// pieces' loads in flight), and writes its four rows of one column straight
+// to the output.
+constexpr int kFixSplit = 32;
+constexpr int kFixInflight = 8;
 
 template <bool GATED>
 __global__ __launch_bounds__(kGemmThreads) void gemm_fixup_kernel(GemmParams p, const char* ws, int P) {
     using C = DmaCfg<GATED>;
     __shared__ __align__(16) char sched[C::SCHED];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int b = blockIdx.y, qs = blockIdx.x;  // the slices of one tile launch together
-    if (b == 0) return;
-    // the tile count first, by a plain sum (most workgroups own nothing and
-    // leave before the schedule's scan)
-    __shared__ int s_wsum[kGemmThreads / 64];
-    int cnt = 0;
-    if (tid < p.n_seg) {
-        const int beg = min(max(p.offsets[tid], 0), p.rows_cap);
-        const int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
-        cnt = ceil_div(end - beg, C::BM);
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
-    if (lane == 0) s_wsum[wave] = cnt;
-    __syncthreads();
-    const int total_mt = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
-    const int nk = p.K / C::BK;
-    const SkSplit sk = sk_split(total_mt * ceil_div(p.N, C::BN), nk, P, true, p.sk_min_idle);
-    const int q = b * sk.share;
-    if (q >= sk.W || q % nk == 0) return;
-    const int t = q / nk;
-    if (b != t * nk / sk.share + 1) return;  // not the first boundary inside tile t
     const TileSched ts = tile_sched(p, sched, C::BM, C::BN);
-    const int p0 = t * nk / sk.share, p1 = ((t + 1) * nk - 1) / sk.share;
-    const TileCoord tc = tile_coord(ts, p.n_seg, sk.F * P + t, C::BM, C::BN);
+    const int nk = p.K / C::BK;
+    const SkSplit sk = sk_split(ts.total_mt * ts.NT, nk, P, true, p.sk_min_idle);
+    const int nsplit = sk.W / nk;  // tiles of the split range
     constexpr int NQ = C::MB * C::NB * 4;  // float4 slots of one matrix per thread
     static_assert(NQ % kFixSplit == 0, "slices of whole slots");
     constexpr int QPER = NQ / kFixSplit;
     const int wm = wave >> 1, wn = wave & 1;
-    // all slots of this slice, piece after piece (every element still sums the
-    // pieces in order); four pieces' loads in flight per step
-    float4 sum[QPER][C::NMAT];
-#pragma unroll
-    for (int k = 0; k < QPER; ++k)
-#pragma unroll
-        for (int mat = 0; mat < C::NMAT; ++mat) sum[k][mat] = make_float4(0.f, 0.f, 0.f, 0.f);
-    auto piece = [&](int pw) {
-        const int slot = pw * sk.share >= t * nk ? 0 : 1;  // share starts inside tile t, or ends in it
-        return (const float4*)(ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
-    };
-    auto add = [&](float4& a, const float4& v) {
-        a.x += v.x;
-        a.y += v.y;
-        a.z += v.z;
-        a.w += v.w;
-    };
-    int pw = p0;
-    for (; pw + 3 <= p1; pw += 4) {
-        float4 v[4][QPER][C::NMAT];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float4* d = piece(pw + j);
-#pragma unroll
-            for (int k = 0; k < QPER; ++k)
-#pragma unroll
-                for (int mat = 0; mat < C::NMAT; ++mat) v[j][k][mat] = d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid];
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int k = 0; k < QPER; ++k)
-#pragma unroll
-                for (int mat = 0; mat < C::NMAT; ++mat) add(sum[k][mat], v[j][k][mat]);
-    }
-    for (; pw <= p1; ++pw) {
-        const float4* d = piece(pw);
+    for (int item = blockIdx.x; item < nsplit * kFixSplit; item += gridDim.x) {
+        const int t = item / kFixSplit, qs = item % kFixSplit;
+        // the first share boundary after the tile's start
+        const int q = (t * nk / sk.share + 1) * sk.share;
+        if (q >= (t + 1) * nk) continue;  // no boundary inside: computed whole
+        const int p0 = t * nk / sk.share, p1 = ((t + 1) * nk - 1) / sk.share;
+        const TileCoord tc = tile_coord(ts, p.n_seg, sk.F * P + t, C::BM, C::BN);
+        float4 sum[QPER][C::NMAT];
 #pragma unroll
         for (int k = 0; k < QPER; ++k)
 #pragma unroll
-            for (int mat = 0; mat < C::NMAT; ++mat) add(sum[k][mat], d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid]);
-    }
+            for (int mat = 0; mat < C::NMAT; ++mat) sum[k][mat] = make_float4(0.f, 0.f, 0.f, 0.f);
+        auto piece = [&](int pw) {
+            const int slot = pw * sk.share >= t * nk ? 0 : 1;  // share starts inside tile t, or ends in it
+            return (const float4*)(ws + ((size_t)2 * pw + slot) * kSkSlotBytes);
+        };
+        auto add = [&](float4& a, const float4& v) {
+            a.x += v.x;
+            a.y += v.y;
+            a.z += v.z;
+            a.w += v.w;
+        };
+        int pw = p0;
+        for (; pw + kFixInflight - 1 <= p1; pw += kFixInflight) {
+            float4 v[kFixInflight][QPER][C::NMAT];
 #pragma unroll
-    for (int k = 0; k < QPER; ++k) {
-        const int qq = qs * QPER + k;  // slot (mb, nb, i4) in the order of store_piece
-        const int i4 = qq & 3, nb = (qq >> 2) % C::NB, mb = (qq >> 2) / C::NB;
-        const int r0 = dma_arow<C>(wm, mb) + 8 * i4 + 4 * (lane >> 5);
-        const int gn = tc.n0 + wn * C::WTN + nb * 32 + (lane & 31);
-        const float g4[4] = {sum[k][0].x, sum[k][0].y, sum[k][0].z, sum[k][0].w};
-        const float4 u = sum[k][C::NMAT - 1];
-        const float u4[4] = {u.x, u.y, u.z, u.w};
+            for (int j = 0; j < kFixInflight; ++j) {
+                const float4* d = piece(pw + j);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float v = GATED ? silu_mul(g4[j], u4[j]) : g4[j];
-            const int gm = tc.m0 + r0 + j;
-            if (gm < tc.m_end && gn < p.N) p.C[(size_t)gm * p.N + gn] = (uint16_t)pack_bf16x2_hw(v, 0.f);
+                for (int k = 0; k < QPER; ++k)
+#pragma unroll
+                    for (int mat = 0; mat < C::NMAT; ++mat)
+                        v[j][k][mat] = d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid];
+            }
+#pragma unroll
+            for (int j = 0; j < kFixInflight; ++j)
+#pragma unroll
+                for (int k = 0; k < QPER; ++k)
+#pragma unroll
+                    for (int mat = 0; mat < C::NMAT; ++mat) add(sum[k][mat], v[j][k][mat]);
+        }
+        for (; pw <= p1; ++pw) {
+            const float4* d = piece(pw);
+#pragma unroll
+            for (int k = 0; k < QPER; ++k)
+#pragma unroll
+                for (int mat = 0; mat < C::NMAT; ++mat)
+                    add(sum[k][mat], d[(mat * NQ + qs * QPER + k) * kGemmThreads + tid]);
+        }
+#pragma unroll
+        for (int k = 0; k < QPER; ++k) {
+            const int qq = qs * QPER + k;  // slot (mb, nb, i4) in the order of store_piece
+            const int i4 = qq & 3, nb = (qq >> 2) % C::NB, mb = (qq >> 2) / C::NB;
+            const int r0 = dma_arow<C>(wm, mb) + 8 * i4 + 4 * (lane >> 5);
+            const int gn = tc.n0 + wn * C::WTN + nb * 32 + (lane & 31);
+            const float g4[4] = {sum[k][0].x, sum[k][0].y, sum[k][0].z, sum[k][0].w};
+            const float4 u = sum[k][C::NMAT - 1];
+            const float u4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float v = GATED ? silu_mul(g4[j], u4[j]) : g4[j];
+                const int gm = tc.m0 + r0 + j;
+                if (gm < tc.m_end && gn < p.N) p.C[(size_t)gm * p.N + gn] = (uint16_t)pack_bf16x2_hw(v, 0.f);
+            }
         }
     }
 }
@@ -1157,8 +1146,7 @@ hipError_t launch_gemm_dma(const GemmParams& g0, void* ws, size_t ws_bytes, hipS
                            split ? (char*)ws : (char*)nullptr);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess || !split) return e;
-        hipLaunchKernelGGL((gemm_fixup_kernel<GATED>), dim3(kFixSplit, P), dim3(kGemmThreads), 0, s, g,
-                           (const char*)ws, P);
+        hipLaunchKernelGGL((gemm_fixup_kernel<GATED>), dim3(P), dim3(kGemmThreads), 0, s, g, (const char*)ws, P);
         return hipGetLastError();
     }
     const int64_t mt_max = ceil_div64(g.rows_cap, C::BM) + g.n_seg;
