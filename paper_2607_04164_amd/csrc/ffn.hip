@@ -1035,10 +1035,25 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_fixup_kernel(GemmParams p, 
     using C = DmaCfg<GATED>;
     __shared__ __align__(16) char sched[C::SCHED];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const TileSched ts = tile_sched(p, sched, C::BM, C::BN);
+    // the tile count first, by a plain sum: with nothing split every
+    // workgroup leaves before the schedule's scan
+    __shared__ int s_wsum[kGemmThreads / 64];
+    int cnt = 0;
+    if (tid < p.n_seg) {
+        const int beg = min(max(p.offsets[tid], 0), p.rows_cap);
+        const int end = min(max(p.offsets[tid + 1], beg), p.rows_cap);
+        cnt = ceil_div(end - beg, C::BM);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if (lane == 0) s_wsum[wave] = cnt;
+    __syncthreads();
+    const int total_mt = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
     const int nk = p.K / C::BK;
-    const SkSplit sk = sk_split(ts.total_mt * ts.NT, nk, P, true, p.sk_min_idle);
+    const SkSplit sk = sk_split(total_mt * ceil_div(p.N, C::BN), nk, P, true, p.sk_min_idle);
     const int nsplit = sk.W / nk;  // tiles of the split range
+    if (nsplit == 0 || (int)blockIdx.x >= nsplit * kFixSplit) return;
+    const TileSched ts = tile_sched(p, sched, C::BM, C::BN);
     constexpr int NQ = C::MB * C::NB * 4;  // float4 slots of one matrix per thread
     static_assert(NQ % kFixSplit == 0, "slices of whole slots");
     constexpr int QPER = NQ / kFixSplit;
