@@ -197,16 +197,17 @@ __global__ __launch_bounds__(kSkThreads, 1) void skinny_gemm_kernel(SkinnyParams
 // chunk earlier, so each chunk waits for most of a memory latency. Here the
 // activation rows and the workgroup's weight rows of a 64-column chunk are
 // copied with global_load_lds (one 128-byte line per row and copy row, 1 KB
-// per instruction) into a ring of slots, NSL-1 chunks ahead, and both MFMA
-// operands are read from LDS. A slot row's 16-byte pieces are XOR-swizzled by
-// (row & 7), so the 8 rows of a read group fall on different banks. One
-// barrier per two chunks: after it every wave's copies of both have landed
-// and every wave has finished reading the slots the next copies overwrite.
-// Decode-shaped (8 segments, d = 2048, d_ff = 1408): gate/up 26 -> 21 us,
-// down 14.0 -> 13.5 us. Reading the next chunk's fragments during the
-// current chunk's MFMAs measured slower; what bounds the kernel now is
-// likelier the access pattern (each weight row is read 128 bytes at a time,
-// K/64 visits per row) than the per-chunk steps.
+// per instruction) into a ring of slots, up to NSL-2 chunks ahead of the two
+// being multiplied, and both MFMA operands are read from LDS. A slot row's
+// 16-byte pieces are XOR-swizzled by (row & 7), so the 8 rows of a read
+// group fall on different banks. One barrier per two chunks: after it every
+// wave's copies of both have landed and every wave has finished reading the
+// slots the next copies overwrite. Decode-shaped (8 segments, d = 2048,
+// d_ff = 1408): gate/up 26 -> 21 us, down 14.0 -> 13.5 us with one barrier
+// per chunk, then 18.0 and 11.6 us with two (the copy loop alone streams the
+// weights at the rate of plain streaming probes; the fragment reads and
+// MFMAs between barriers were what it lost). Reading the next chunk's
+// fragments during the current chunk's MFMAs measured slower.
 constexpr int kS2KC = 64;             // K columns per chunk
 constexpr int kS2RowB = kS2KC * 2;    // bytes per slot row (one 128-byte line)
 
