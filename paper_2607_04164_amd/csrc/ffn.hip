@@ -380,14 +380,23 @@ __device__ __forceinline__ int swz(int row) { return (row >> 1) & (KC - 1); }
 template <class C>
 __device__ __forceinline__ int lds_off(int r, int c) { return r * C::ROW_BYTES + ((c ^ swz<C::KC>(r)) << 4); }
 
+// Zero-filled rows (device memory of the library, zero at load time): the
+// copies of A rows wholly past a segment's end read these instead of the
+// segment's last row, so the MFMAs of padding rows see zero operands.
+constexpr int kZeroBytes = 64 * 1024 + 128;
+__device__ __align__(256) uint16_t g_zero_rows[kZeroBytes / 2];
+
 // Copy sources of one wave: a workgroup-uniform base per operand (SGPRs) and
-// a 32-bit byte offset per lane and instruction (one VGPR each).
+// a 32-bit byte offset per lane and instruction (one VGPR each). Bit i of
+// a_zero: A instruction i's rows all lie past the segment's end (it copies
+// from g_zero_rows).
 template <class C>
 struct DmaSrc {
     const char* a_base;
     const char* b_base;
     uint32_t a_off[C::A_DMA];
     uint32_t b_off[C::B_DMA];
+    int a_zero;
 };
 
 // DMA instruction i of the wave's share of a K-step: instructions 0..A_DMA-1
@@ -396,8 +405,8 @@ struct DmaSrc {
 template <class C>
 __device__ __forceinline__ void dma_one(const DmaSrc<C>& src, uint32_t stage_lds, int wave, int kb, int i) {
     if (i < C::A_DMA) {
-        dma16s(src.a_base + kb, src.a_off[i],
-               stage_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
+        const char* base = (src.a_zero >> i) & 1 ? (const char*)g_zero_rows : src.a_base;
+        dma16s(base + kb, src.a_off[i], stage_lds + ((wave * C::A_DMA + i) * C::ROWS_PER_DMA) * C::ROW_BYTES);
     } else {
         const int j = i - C::A_DMA;
         dma16s(src.b_base + kb, src.b_off[j],
@@ -561,12 +570,20 @@ __device__ __forceinline__ void dma_sources(DmaSrc<C>& src, const GemmParams& p,
     // rows are gathered (the host keeps a_count * K * 2 below 2^32)
     const int base_row = p.a_rows ? 0 : tc.m0;
     src.a_base = (const char*)(p.A + (size_t)base_row * K);
+    // an instruction whose rows all lie past the segment's end copies zeros
+    // (row stride 0 into g_zero_rows, which holds a whole row of K columns)
+    const bool zero_ok = (size_t)K * 2 + 128 <= (size_t)kZeroBytes;
+    int a_zero = 0;
 #pragma unroll
     for (int i = 0; i < C::A_DMA; ++i) {
         const int r = (wave * C::A_DMA + i) * C::ROWS_PER_DMA + lrow;
+        const bool z = zero_ok && tc.m0 + (wave * C::A_DMA + i) * C::ROWS_PER_DMA >= tc.m_end;
+        a_zero |= z ? 1 << i : 0;
         const int row = gathered_row(p.a_rows, p.a_count, min(tc.m0 + r, tc.m_end - 1));
-        src.a_off[i] = (uint32_t)(((size_t)(row - base_row) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
+        src.a_off[i] = z ? (uint32_t)(lchk << 4)
+                         : (uint32_t)(((size_t)(row - base_row) * K + ((lchk ^ swz<C::KC>(r)) << 3)) * 2);
     }
+    src.a_zero = __builtin_amdgcn_readfirstlane(a_zero);
     // a wave's B rows lie in one matrix (gate or up for the gated GEMM)
     static_assert(!GATED || (C::B_DMA * C::ROWS_PER_DMA * 2 == C::BN), "B rows of a wave in one matrix");
     const int bmat = GATED ? (wave * C::B_DMA * C::ROWS_PER_DMA) / C::BN : 0;
