@@ -3,13 +3,15 @@
 One step = one full layer forward over one batch of synthetic tokens, every
 stage on the GPU: route (gate logits, softmax, top-k, expert-to-group map,
 per-group merge) -> dispatch (group histogram, decoupled look-back scan,
-row gather) -> FFN gate/up grouped GEMM -> FFN down grouped GEMM
-[-> shared-expert FFN] -> combine. Inputs and weights are resident in HBM
-before the timed region; nothing is allocated inside it.
+row gather) -> FFN gate/up grouped GEMM -> FFN down grouped GEMM -> combine,
+with the shared-expert FFN (layers that have one) on the layer's side stream
+from the start of the step, joined before the combine. Inputs and weights are
+resident in HBM before the timed region; nothing is allocated inside it.
 
 Prints one JSON line. `value` is layer tokens/s over the K timed steps;
 `roofline` is for the dominant kernel (the fused gate/up grouped GEMM) from
-HIP events around its launches inside the timed steps; `stages` gives every
+HIP events around its launches inside the timed steps (with shared experts,
+from the per-stage pass, where it runs alone); `stages` gives every
 stage's average time and achieved rate against its own roofline;
 `cpu_baseline` times the CPU oracle on a bounded token sample.
 
@@ -260,20 +262,34 @@ def time_layer(cfg, args, dev, device_weights=False):
              "shared_ffn": lambda: layer.shared(x), "combine": layer.combine,
              "down_combine": layer.down_combine if fold else None}
 
-    def step(events=None):
-        for i, s in enumerate(stages):
-            if events is not None:
-                events[i].record()
-            calls[s]()
-        if events is not None:
-            events[-1].record()
+    # the layer's own schedule (LayerForward's order): with shared experts the
+    # shared FFN starts on the layer's side stream first and joins before the
+    # combine; the per-stage breakdown below runs the stages one after another
+    # on one stream instead, so each is timed alone
+    order = list(stages)
+    if cfg.n_shared and layer._side is not None:
+        order.remove("shared_ffn")
+        order.insert(0, "shared_fork")
+        order.insert(order.index("down_combine" if fold else "combine"), "shared_join")
+    calls["shared_fork"] = lambda: layer.shared_fork(x)
+    calls["shared_join"] = layer.shared_join
 
-    dom_i = stages.index("ffn_gate_up")
+    def step(events=None):
+        if events is None:
+            for s in order:
+                calls[s]()
+            return
+        for i, s in enumerate(stages):
+            events[i].record()
+            calls[s]()
+        events[-1].record()
+
+    dom_i = order.index("ffn_gate_up")
 
     def timed_step(e0, e1):
         # the headline steps: events only around the dominant kernel, so the
         # host work per step stays the library calls
-        for i, s in enumerate(stages):
+        for i, s in enumerate(order):
             if i == dom_i:
                 e0.record()
                 calls[s]()
@@ -305,6 +321,11 @@ def time_layer(cfg, args, dev, device_weights=False):
     torch.cuda.synchronize()
     per_stage_ms = {s: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
                     for i, s in enumerate(stages)}
+    if order != stages:
+        # the timed steps ran the shared FFN beside the routed GEMMs, so their
+        # events around the gate/up GEMM hold a shared GPU: its rate comes from
+        # this pass, where it runs alone
+        dom_ms = per_stage_ms["ffn_gate_up"]
     # the same step captured once into a HIP graph and replayed: the steps'
     # kernels without the host's launch work (wall clock over the replays)
     graph_ms = None
@@ -507,7 +528,7 @@ def main():
 
     dom = "ffn_gate_up"
     dkind, damount = work[dom]
-    dms = dom_ms  # HIP events around the dominant kernel inside the timed steps
+    dms = dom_ms  # HIP events around the dominant kernel (timed steps, or the per-stage pass)
     # the record holds for the named workload only, not a share or another threshold
     traffic = (recorded_traffic(args.config)
                if share is None and args.theta is None and not args.fused_gather else None)
@@ -553,7 +574,8 @@ def main():
         "roofline": roofline,
         "stages": stage_out,
         "stages_note": "us / rates: the stage launched alone back to back (warm: activations, and weights "
-                       "below 256 MB, may be served from the 256 MB MALL); in_step_us: inside the timed steps; "
+                       "below 256 MB, may be served from the 256 MB MALL); in_step_us: inside a second pass over the "
+                       "steps with events around every stage, one stage after another on one stream; "
                        "cold_*: median launch after a 1 GiB read pass that evicts L2 and the MALL, timed by HIP "
                        "events around the one launch (so it includes the launch and event overhead that "
                        "cold_launch_floor_us measures on a one-workgroup elementwise launch)",

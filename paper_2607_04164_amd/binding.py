@@ -510,10 +510,18 @@ class LayerForward:
     fold_combine=True: the combine runs in the down projection's epilogue
     (brownout_moe_ffn_down_combine; its tiles are never split, so the layer
     equals the unfused layer without the stream-K workspace, bit for bit).
+
+    concurrent_shared=True (layers with shared experts): a forward starts the
+    shared-expert FFN on a side stream of the layer's own (default priority)
+    as soon as x is ready and joins it before the combine; the routed path
+    runs meanwhile on the caller's stream. The shared FFN then runs without
+    the stream-K workspace (whole tiles; with a split its last bits could
+    differ from the one-stream forward, which splits where the workspace
+    allows).
     """
 
     def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True,
-                 fused_gather: bool = False, fold_combine: bool = False):
+                 fused_gather: bool = False, fold_combine: bool = False, concurrent_shared: bool = True):
         self.desc = desc
         self.w = weights
         self.fused_gather = fused_gather
@@ -539,10 +547,14 @@ class LayerForward:
         self.ws = new_dispatch_workspace(desc, device)
         self.ffn_ws = new_ffn_workspace(desc, device) if stream_k else None
         self.fold_ws = new_down_combine_workspace(desc, device) if fold_combine else None
+        self._side = None
         if desc.d_ff_shared:
             self.bufs["h_sh"] = _empty((max(T, 1), desc.d_ff_shared), dt, device)
             self.bufs["y_sh"] = _empty((max(T, 1), d), dt, device)
             self.sh_offsets = torch.tensor([0, T], dtype=torch.int32, device=device)
+            if concurrent_shared:
+                # default priority, as every stream of the layer
+                self._side = torch.cuda.Stream(device=device)
         self._plan()
 
     def _plan(self):
@@ -593,6 +605,9 @@ class LayerForward:
             _dev(w["w_down_sh"], "w_down_sh", dt, (1, d, fs))
             self._shared_args = (dtype, 1, T, d, fs, ptr(self.sh_offsets), ptr(w["w_gate_sh"]),
                                  ptr(w["w_up_sh"]), ptr(w["w_down_sh"]), ptr(b["h_sh"]), ptr(b["y_sh"]), wsp, wsn)
+            # on the side stream without the stream-K workspace, which the
+            # routed FFN may be using at the same time (its tiles stay whole)
+            self._shared_side_args = self._shared_args[:-2] + (None, 0)
 
     def _x(self, x) -> int:
         if not (isinstance(x, torch.Tensor) and x.is_cuda and x.dtype == self._dt
@@ -648,6 +663,27 @@ class LayerForward:
         _check(self._lib.brownout_moe_ffn(*a[:6], x.data_ptr(), *a[6:], self._s(stream)), "brownout_moe_ffn")
         return self.bufs["y_sh"], self.bufs["h_sh"]
 
+    def shared_fork(self, x, stream=None):
+        """Starts the shared experts on the layer's side stream, after the work
+        queued so far on `stream` (x is ready): they read only x, so they run
+        beside route, dispatch and the routed FFN and fill the CUs those leave
+        idle (the persistent GEMMs' partial last rounds, the short kernels).
+        shared_join must follow before y_sh is read. Without a side stream
+        (concurrent_shared=False or no shared experts) this is `shared`."""
+        if self._side is None:
+            return self.shared(x, stream)
+        self._x(x)
+        self._side.wait_stream(stream if stream is not None else torch.cuda.current_stream())
+        a = self._shared_side_args
+        _check(self._lib.brownout_moe_ffn(*a[:6], x.data_ptr(), *a[6:], self._side.cuda_stream),
+               "brownout_moe_ffn")
+        return self.bufs["y_sh"], self.bufs["h_sh"]
+
+    def shared_join(self, stream=None):
+        """Makes `stream` wait for the shared experts started by shared_fork."""
+        if self._side is not None:
+            (stream if stream is not None else torch.cuda.current_stream()).wait_stream(self._side)
+
     def combine(self, stream=None):
         _check(self._lib.brownout_moe_combine(self._desc_ref, *self._combine_args, self._s(stream)),
                "brownout_moe_combine")
@@ -660,14 +696,17 @@ class LayerForward:
         return self.bufs["out"]
 
     def __call__(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        shared = bool(self.desc.d_ff_shared)
+        if shared:
+            self.shared_fork(x, stream)
         self.route(x, stream)
         self.dispatch(x, stream)
         if self.fold_combine:
             self.ffn_gate_up(stream, x=x)
-            if self.desc.d_ff_shared:
-                self.shared(x, stream)
+            if shared:
+                self.shared_join(stream)
             return self.down_combine(stream)
         self.ffn(stream, x=x)
-        if self.desc.d_ff_shared:
-            self.shared(x, stream)
+        if shared:
+            self.shared_join(stream)
         return self.combine(stream)

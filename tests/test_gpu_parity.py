@@ -530,6 +530,39 @@ def test_deterministic_bits():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+@pytest.mark.parametrize("name", ["heavy-s", "dma-shared"])
+def test_shared_side_stream_bit_identical(name):
+    """The shared experts on the layer's side stream (started once x is ready,
+    joined before the combine) give the bits of the one-stream layer, call
+    after call with no synchronisation between the forwards, also when the
+    caller passes a stream of its own; y_sh equals the shared FFN run alone.
+    (Neither shape splits a shared-FFN tile, so the one-stream layer's
+    workspace changes no bit.)"""
+    cfg = SMALL["heavy-s"] if name == "heavy-s" else FOLD["dma-shared"]
+    L = W.make_layer(cfg, 3)
+    w = device_weights(L)
+    x = dev_tensor(L.x, cfg.dtype)
+    one = B.LayerForward(desc_of(cfg), w, concurrent_shared=False)
+    assert one._side is None
+    want = one(x).clone()
+    want_sh = one.bufs["y_sh"].clone()
+    both = B.LayerForward(desc_of(cfg), w)
+    assert both._side is not None
+    outs = []
+    for _ in range(3):
+        outs.append(both(x).clone())
+    caller = torch.cuda.Stream()
+    caller.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(caller):
+        outs.append(both(x, stream=caller).clone())
+    torch.cuda.current_stream().wait_stream(caller)
+    torch.cuda.synchronize()
+    for i, o in enumerate(outs):
+        assert torch.equal(o.view(torch.int16), want.view(torch.int16)), f"forward {i}"
+    assert torch.equal(both.bufs["y_sh"], want_sh)
+    check_layer(L, oracle.layer(L, want_intermediates=True), both, outs[-1])
+
+
 def test_token_order_invariance():
     """Permuting tokens permutes the output rows bit for bit and keeps the counts."""
     L, _ = case("fine-s", 0)
