@@ -97,8 +97,11 @@ def parse():
                     help="instead of the layer forward: time the evaluation of one candidate grouping of the "
                          "workload's layer (parameter-average united experts, their FFN on the T tokens as "
                          "calibration set, the routing-weighted distillation errors)")
+    ap.add_argument("--four-calls", action="store_true",
+                    help="time the four-call path (dispatch writes x_perm) where the layer would take the fused "
+                         "gather (top-3 and above)")
     ap.add_argument("--no-compare-fused", action="store_true",
-                    help="skip the second timing of the same layer on the fused-gather path")
+                    help="skip the second timing of the same layer on the other gather path")
     ap.add_argument("--no-compare-fold", action="store_true",
                     help="skip timing the layer with the combine folded into the down projection")
     ap.add_argument("--theta", type=float, default=None,
@@ -245,10 +248,14 @@ def time_layer(cfg, args, dev, device_weights=False):
     x = to_dev(L.x)
     desc = B.make_desc(cfg.T, cfg.d, cfg.E, cfg.top_k, cfg.G, cfg.d_ff, cfg.d_ff_shared, cfg.norm_topk,
                        cfg.dtype)
-    fused = bool(getattr(args, "fused_gather", False))
+    # the layer's own choice of path unless asked for the fused gather (or the
+    # x_perm rows an expert-parallel share needs)
+    four_calls = getattr(args, "four_calls", False) or bool(share and share[0] == "ep")
+    fused = True if getattr(args, "fused_gather", False) else (False if four_calls else None)
     fold = bool(getattr(args, "fold_combine", False))
     layer = B.LayerForward(desc, w, device=dev, fused_gather=fused, fold_combine=fold,
                            stream_k=not getattr(args, "no_stream_k", False))
+    fused = layer.fused_gather
 
     if fold:
         # the shared experts' output feeds the folded combine
@@ -406,7 +413,8 @@ def time_layer(cfg, args, dev, device_weights=False):
     del flush
     del layer, w, x
     torch.cuda.empty_cache()
-    return L0, (cfg, seg_info, ep_ms, graph_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages
+    return L0, (cfg, seg_info, ep_ms, graph_ms, fused), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, \
+        stages
 
 
 def ungrouped_line(cfg, args, dev, ms_grouped):
@@ -479,7 +487,8 @@ def main():
     torch.cuda.set_device(dev)
     B.load_library()
     cfg0 = cfg
-    L, (cfg, seg_info, ep_ms, graph_ms), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, stages = \
+    L, (cfg, seg_info, ep_ms, graph_ms, path_fused), ms_step, dom_ms, per_stage_ms, iso_ms, cold_ms, N, counts, \
+        stages = \
         time_layer(cfg, args, dev)
     share = parse_share(args.share)
 
@@ -493,7 +502,7 @@ def main():
     work = {
         "route": ("hbm", T * d * s + E * d * s + T * k * 16),
         # fused gather: the permutation only (slot_group in, slot_row and perm_token out)
-        "dispatch": ("hbm", (T * k * 8 + N * 4) if args.fused_gather else
+        "dispatch": ("hbm", (T * k * 8 + N * 4) if path_fused else
                      (T * k * 4 + T * d * s + N * d * s + N * 4 + T * k * 4)),
         "ffn_gate_up": ("hbm", 2 * S_w * d * f * s + N * d * s + N * f * s) if skinny else ("mfma", 4.0 * N * d * f),
         "ffn_down": ("hbm", S_w * d * f * s + N * f * s + N * d * s) if skinny else ("mfma", 2.0 * N * d * f),
@@ -531,7 +540,7 @@ def main():
     dms = dom_ms  # HIP events around the dominant kernel (timed steps, or the per-stage pass)
     # the record holds for the named workload only, not a share or another threshold
     traffic = (recorded_traffic(args.config)
-               if share is None and args.theta is None and not args.fused_gather else None)
+               if share is None and args.theta is None and not path_fused else None)
     if skinny:
         dach = damount / (dms * 1e-3) / 1e9
         cach = damount / (cold_ms[dom] * 1e-3) / 1e9
@@ -587,8 +596,10 @@ def main():
         "cpu_baseline": None,
     }
 
-    if args.fused_gather:
-        result["config"]["fused_gather"] = True
+    # the layer's path: the four calls, or dispatch writing only the
+    # permutation and the gate/up GEMM gathering its rows from x (LayerForward
+    # takes the latter by default from top-3 on)
+    result["config"]["gather"] = "fused" if path_fused else "four calls"
     if seg_info is not None:
         # G above is the united-expert count; the layer ran over the segments
         result["config"]["partial_brownout"] = seg_info
@@ -611,7 +622,15 @@ def main():
                                 "note": "each rank's grouped FFN (gate/up + down) over its block, "
                                         "on the rows the whole dispatch gave it; exchange not timed"}
 
-    if not args.fused_gather and not args.no_compare_fused and share is None:
+    if path_fused and not args.fused_gather and not args.no_compare_fused and share is None:
+        # the same layer on the four-call path (bit-identical results)
+        nargs = argparse.Namespace(**{**vars(args), "four_calls": True})
+        _, _, ms_n, _, _, iso_n, _, _, _, _ = time_layer(cfg0, nargs, dev)
+        result["four_calls"] = {"value": round(cfg.T / (ms_n * 1e-3), 1), "ms_per_step": round(ms_n, 4),
+                                "stages_us": {k: round(v * 1e3, 2) for k, v in iso_n.items()},
+                                "fused_speedup": round(ms_n / ms_step, 3),
+                                "note": "dispatch writes x_perm and the gate/up GEMM reads it"}
+    if not path_fused and not args.no_compare_fused and share is None:
         # the same layer on the fused-gather path (bit-identical results)
         fargs = argparse.Namespace(**{**vars(args), "fused_gather": True})
         _, _, ms_f, _, stages_f, iso_f, _, _, _, _ = time_layer(cfg0, fargs, dev)
@@ -649,10 +668,11 @@ def main():
         for name in ("fine", "heavy", "decode"):
             wcfg = W.CONFIGS[name]
             xargs = argparse.Namespace(**{**vars(args), "share": None, "fused_gather": False})
-            _, (_, _, _, graph_w), ms_w, dom_w, _, iso_w, cold_w, N_w, counts_w, _ = \
+            _, (_, _, _, graph_w, fused_w), ms_w, dom_w, _, iso_w, cold_w, N_w, counts_w, _ = \
                 time_layer(wcfg, xargs, dev, device_weights=True)
             line = {"workload": WORKLOAD_TEXT[name], "value": round(wcfg.T / (ms_w * 1e-3), 1),
                     "unit": "tokens/s", "ms_per_step": round(ms_w, 4),
+                    "gather": "fused" if fused_w else "four calls",
                     "graph_ms_per_step": None if graph_w is None else round(graph_w, 4), "rows_N": N_w,
                     "dominant": dominant_rate(wcfg, N_w, counts_w, dom_w, cold_w["ffn_gate_up"]),
                     "stages_us": {k: round(v * 1e3, 2) for k, v in iso_w.items()},

@@ -490,6 +490,10 @@ def ffn_down_combine(desc: Desc, offsets, h, w_down, perm_token, slot_row, slot_
 
 # ---------------------------------------------------------------------------
 
+# top_k from which LayerForward takes the fused gather by default
+FUSED_GATHER_MIN_TOP_K = 3
+
+
 class LayerForward:
     """One grouped MoE layer with its weights and every intermediate buffer
     allocated once, so a forward enqueues only the library's kernels.
@@ -505,7 +509,12 @@ class LayerForward:
 
     fused_gather=True: dispatch writes only the permutation and the gate/up
     GEMM gathers its rows from x (no x_perm buffer); ffn and ffn_gate_up then
-    take x. Results are bit-identical to the unfused path.
+    take x. Results are bit-identical to the unfused path. None (the default)
+    takes it when top_k >= FUSED_GATHER_MIN_TOP_K: x_perm then holds top_k
+    copies of x's rows, and writing and re-reading it costs more than the
+    GEMM's row gather (fine, heavy, decode and partial-brownout workloads,
+    top-4 and top-6: layer 2-4 % faster); at top-2 the two paths time alike
+    and the four calls are kept.
 
     fold_combine=True: the combine runs in the down projection's epilogue
     (brownout_moe_ffn_down_combine; its tiles are never split, so the layer
@@ -521,10 +530,12 @@ class LayerForward:
     """
 
     def __init__(self, desc: Desc, weights: Dict[str, torch.Tensor], device="cuda", stream_k: bool = True,
-                 fused_gather: bool = False, fold_combine: bool = False, concurrent_shared: bool = True):
+                 fused_gather: Optional[bool] = None, fold_combine: bool = False, concurrent_shared: bool = True):
         self.desc = desc
         self.w = weights
-        self.fused_gather = fused_gather
+        if fused_gather is None:
+            fused_gather = desc.top_k >= FUSED_GATHER_MIN_TOP_K
+        self.fused_gather = bool(fused_gather)
         self.fold_combine = fold_combine
         _check(validate(desc), "bmoe_validate")
         T, k, d, G, E = desc.T, desc.top_k, desc.d, desc.G, desc.E

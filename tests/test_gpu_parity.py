@@ -634,12 +634,16 @@ def test_ffn_gather_bit_identical(name, stream_k):
 @pytest.mark.parametrize("name", ["fine-s", "heavy-s", "tail"])
 def test_layer_fused_gather(name):
     """The fused-gather layer: bit-identical to the four-call layer, and
-    within tolerance of the oracle."""
+    within tolerance of the oracle. The default layer takes the fused gather
+    from top-3 on."""
     L, ref = case(name, 0)
     cfg = L.cfg
     w = device_weights(L)
     x = dev_tensor(L.x, cfg.dtype)
-    out0 = B.LayerForward(desc_of(cfg), w)(x).clone()
+    assert B.LayerForward(desc_of(cfg), w).fused_gather == (cfg.top_k >= B.FUSED_GATHER_MIN_TOP_K)
+    four = B.LayerForward(desc_of(cfg), w, fused_gather=False)
+    assert "x_perm" in four.bufs["dispatch"]
+    out0 = four(x).clone()
     layer = B.LayerForward(desc_of(cfg), w, fused_gather=True)
     out1 = layer(x)
     torch.cuda.synchronize()
@@ -651,13 +655,16 @@ def test_layer_fused_gather(name):
 @pytest.mark.parametrize("name", ["mixtral", "fine", "heavy", "decode"])
 def test_full_size_fused_gather_bit_identical(name):
     """At full size and with the stream-K workspace, the fused-gather layer
-    writes the same bits as the four-call layer (whose parity with the oracle
-    test_full_size_sampled checks)."""
+    writes the same bits as the four-call layer. test_full_size_sampled checks
+    the default layer against the oracle (four calls at top-2, the fused
+    gather from top-3 on), so this ties the other path to it."""
     L = full_case(name)
     cfg = L.cfg
     w = device_weights(L)
     x = dev_tensor(L.x, cfg.dtype)
-    out0 = B.LayerForward(desc_of(cfg), w)(x).clone()
+    four = B.LayerForward(desc_of(cfg), w, fused_gather=False)
+    assert "x_perm" in four.bufs["dispatch"]
+    out0 = four(x).clone()
     layer = B.LayerForward(desc_of(cfg), w, fused_gather=True)
     out1 = layer(x)
     torch.cuda.synchronize()
