@@ -242,13 +242,14 @@ BMOE_API bmoe_status brownout_moe_dispatch_noalloc(const bmoe_desc* desc, const 
  * block of united experts under expert parallelism); other rows stay untouched.
  * The shared experts of a layer run through this call too, with n_seg = 1,
  * offsets = {0, T}, a = x.
- * workspace (optional, device memory, 256-byte aligned): NULL runs one output
- * tile per workgroup. With at least bmoe_workspace_bytes(desc,
- * BMOE_STAGE_FFN) bytes (the size depends on the current device) the large
- * bf16 GEMMs run one workgroup per CU and split the K loop of the last tiles
- * so every CU gets the same work; the partial sums of a split tile meet in
- * the workspace in a fixed order, so results stay deterministic (they may
- * differ in the last bits from the NULL-workspace path). Contents need no
+ * workspace (optional, device memory, 256-byte aligned): the large bf16
+ * GEMMs run one workgroup per CU, each taking whole output tiles in turn;
+ * NULL keeps every tile whole. With at least bmoe_workspace_bytes(desc,
+ * BMOE_STAGE_FFN) bytes (the size depends on the current device) they may
+ * also split the K loop of the last tiles so every CU gets the same work;
+ * the partial sums of a split tile meet in the workspace in a fixed order,
+ * so results stay deterministic (they may differ in the last bits from the
+ * NULL-workspace path). Contents need no
  * initialisation and are not preserved; calls that can overlap in time must
  * not share a workspace. A non-NULL workspace below the size is
  * BMOE_ERR_WORKSPACE. The K loops are split only when whole tiles would leave
