@@ -23,7 +23,11 @@
  *
  * Conventions for every call:
  *   - Tensor pointers are DEVICE pointers, row-major, owned by the caller. The
- *     library allocates nothing, frees nothing and keeps no state.
+ *     library allocates and frees nothing at run time. Its only device memory
+ *     is two fixed arrays of its code object, one copy per GPU: 64 KiB of
+ *     zeros that the FFN's copies of padding rows read, and the workspace of
+ *     brownout_moe_dispatch_noalloc. On the host it caches per-device facts
+ *     (CU count, those arrays' addresses, kernel attributes set once).
  *   - Weights use the [out, in] layout: W_gate/W_up [n, d_ff, d], W_down [n, d, d_ff].
  *   - Every call checks its arguments on the host before it enqueues anything;
  *     on error it returns a BMOE_ERR_* code and writes nothing. Launch failures
