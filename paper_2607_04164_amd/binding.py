@@ -510,7 +510,8 @@ class LayerForward:
     fused_gather=True: dispatch writes only the permutation and the gate/up
     GEMM gathers its rows from x (no x_perm buffer); ffn and ffn_gate_up then
     take x. Results are bit-identical to the unfused path. None (the default)
-    takes it when top_k >= FUSED_GATHER_MIN_TOP_K: x_perm then holds top_k
+    takes it when top_k >= FUSED_GATHER_MIN_TOP_K (and x is below 4 GiB, the
+    gather's addressing limit): x_perm then holds top_k
     copies of x's rows, and writing and re-reading it costs more than the
     GEMM's row gather (fine, heavy, decode and partial-brownout workloads,
     top-4 and top-6: layer 2-4 % faster); at top-2 the two paths time alike
@@ -534,7 +535,9 @@ class LayerForward:
         self.desc = desc
         self.w = weights
         if fused_gather is None:
-            fused_gather = desc.top_k >= FUSED_GATHER_MIN_TOP_K
+            # (the gathered copies address x with 32-bit byte offsets)
+            x_bytes = desc.T * desc.d * (2 if desc.dtype == BMOE_BF16 else 4)
+            fused_gather = desc.top_k >= FUSED_GATHER_MIN_TOP_K and x_bytes < (1 << 32)
         self.fused_gather = bool(fused_gather)
         self.fold_combine = fold_combine
         _check(validate(desc), "bmoe_validate")
