@@ -33,6 +33,9 @@ SMALL = {
     "heavy-s": W.CONFIGS["heavy"].with_(name="heavy-s", T=700, d=512, d_ff=192, d_ff_shared_each=192),
     "decode": W.CONFIGS["decode"],
     "tail": W.LayerConfig("tail", T=33, d=264, E=12, top_k=3, G=5, d_ff=520, dtype="bf16", zipf_s=1.2),
+    # d_ff not a whole 64-column K-step: the register-staged 128-row tiles
+    # (whole 64-column K-steps take the persistent 256-row kernel at any size)
+    "ragged-s": W.CONFIGS["mixtral"].with_(name="ragged-s", T=300, d=520, d_ff=600),
 }
 CASES = [(n, 0) for n in SMALL] + [("tiny", 1), ("tiny", 2), ("fine-s", 1)]
 IDS = [f"{n}-seed{s}" for n, s in CASES]
@@ -592,7 +595,8 @@ def partial_layer(L):
 
 GATHER = {
     "tiny": SMALL["tiny"],                     # fp32 kernels
-    "mixtral-s": SMALL["mixtral-s"],           # 128-row register-staged tiles
+    "mixtral-s": SMALL["mixtral-s"],           # persistent 256-row tiles, 150 rows per group
+    "ragged-s": SMALL["ragged-s"],             # 128-row register-staged tiles
     "decode": SMALL["decode"],                 # skinny weight-streaming kernels
     "dma": W.LayerConfig("dma", T=2100, d=256, E=8, top_k=2, G=4, d_ff=384, dtype="bf16", zipf_s=0.5),
 }
@@ -680,8 +684,9 @@ FOLD = {
     "dma-k1": W.LayerConfig("dma-k1", T=4500, d=384, E=8, top_k=1, G=4, d_ff=256, dtype="bf16", zipf_s=0.5),
     "dma-shared": W.LayerConfig("dma-shared", T=1200, d=256, E=16, top_k=6, G=4, d_ff=256, dtype="bf16",
                                 zipf_s=1.5, n_shared=2, d_ff_shared_each=128),
+    "mixtral-s": SMALL["mixtral-s"],  # the persistent kernel with 150 rows per group
     # other shapes: the down projection, then the combine kernel
-    "mixtral-s": SMALL["mixtral-s"],
+    "ragged-s": SMALL["ragged-s"],
     "tiny": SMALL["tiny"],
 }
 
