@@ -40,8 +40,8 @@ VALU_F32_PEAK_TFLOPS = 157.3
 # --copy-probe-mib 1024: FETCH_SIZE reads half the copied bytes, WRITE_SIZE
 # all of them). Valid only for the kernel sources they were taken with.
 TRAFFIC_RECORDS = {
-    "mixtral": {"src_sha1": "821a3ecb0beb493faa9eba0d01212fa4fc84e90a",
-                "fetch_kib": 1523132.4, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "mixtral": {"src_sha1": "2efdf76e76bd4d124a9ba69e7eaa1ca11afd732e",
+                "fetch_kib": 1524119.3, "write_kib": 217336.0, "fetch_scale": 2.0, "write_scale": 1.0,
                 "profile": "profiles/gemm_gate_up_mixtral_hbm_counters.md"},
 }
 TRAFFIC_SOURCES = ("paper_2607_04164_amd/csrc/ffn.hip", "paper_2607_04164_amd/csrc/bmoe_common.h")
