@@ -326,10 +326,17 @@ def test_ffn_skinny_paths(sizes, spare, d, f):
     assert_close_rows(host_f32(yg[:N]), ref_y, "bf16", "y")
 
 
+# 60 segments of skewed sizes (1/rank), every seventh empty: ~200 rows per
+# segment on average, the many small groups of an ungrouped layer
+_SIZES60 = tuple(0 if i % 7 == 0 else 3000 // (i + 1) for i in range(60))
+
 LARGE_TILE_FFN = [
-    # (segment sizes, rows_cap, d, d_ff): rows_cap >= 1024 * segments selects the
-    # 256-row tiles; d and d_ff multiples of 64 select the direct-to-LDS kernels
+    # (segment sizes, rows_cap, d, d_ff): above the skinny kernels' size, d and
+    # d_ff multiples of 64 select the persistent direct-to-LDS kernel at any
+    # group size; otherwise rows_cap >= 1024 * segments selects the register-
+    # staged 256-row tiles
     ((700, 333), 2048, 256, 384),
+    (_SIZES60, sum(_SIZES60) + 300, 256, 192),
     ((1000, 0, 513, 1), 4096, 320, 448),   # N tails in both GEMMs, empty and 1-row segments
     ((0, 1290), 2048, 512, 192),
     ((1000, 0, 513, 1), 4096, 288, 352),   # not multiples of 64: register-staged 256-row kernels
