@@ -869,6 +869,23 @@ def test_full_size_sampled(name):
         assert n_split > 0
 
 
+@pytest.mark.parametrize("name", ["partial-theta1", "fine-ungrouped"])
+def test_full_size_many_groups(name):
+    """Full-size fine-grained layers with 60 small, skewed groups (about 530
+    rows each on average): zero brownout over the segment map (theta 1, every
+    expert on its own FFN) and the layer with G = E. They run the persistent
+    256-row GEMM like the grouped layers; integers in full, floats sampled."""
+    if name == "partial-theta1":
+        L = partial_layer(W.make_layer(W.CONFIGS["partial"].with_(name="partial-theta1", theta=1.0), 0))
+    else:
+        cfg = W.CONFIGS["fine"]
+        L = W.make_layer(cfg.with_(name="fine-ungrouped", G=cfg.E), 0)
+    assert len(np.asarray(L.e2g).tolist()) == 60 and len(set(np.asarray(L.e2g).tolist())) == 60
+    layer, out = run_layer(L)
+    _, dsp, _ = _check_full_size(L, layer, out, 48, seed=3)
+    _check_split_tiles(L, layer, dsp)
+
+
 def test_full_size_fold_combine_bit_identical():
     """The Mixtral-shaped layer with the combine folded into the down
     projection writes the same out bits as the unfused layer without the
